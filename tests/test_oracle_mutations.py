@@ -1,0 +1,187 @@
+"""Plant plausible mistakes in the oracle (on the CPU) and show that a pin
+catches each one.  Every mutation is a copy of an oracle module with one
+function replaced; the real oracle is never modified."""
+import copy
+import math
+import types
+
+import numpy as np
+import pytest
+
+import oracle.par as P
+import oracle.route as R
+import oracle.attn as A
+import test_oracle_par as TP
+import test_oracle_route_attn as TR
+
+
+def clone(mod, **repl):
+    m = types.ModuleType(mod.__name__ + "_mut")
+    m.__dict__.update(copy.copy(mod.__dict__))
+    m.__dict__.update(repl)
+    # rebind module-level functions so internal calls see the replacements
+    for name, obj in list(m.__dict__.items()):
+        if isinstance(obj, types.FunctionType) and obj.__module__ == mod.__name__ and name not in repl:
+            m.__dict__[name] = types.FunctionType(obj.__code__, m.__dict__, name,
+                                                  obj.__defaults__, obj.__closure__)
+    return m
+
+
+def _cross_no_conj(Fa, Fb):
+    return (Fb * Fa).sum(-1), (np.abs(Fb) * np.abs(Fa)).sum(-1)
+
+
+def _cross_swapped(Fa, Fb):
+    return (Fa * np.conj(Fb)).sum(-1), (np.abs(Fb) * np.abs(Fa)).sum(-1)
+
+
+def _blend_sign(Fa, Fb, theta, gate, alpha):
+    ua = np.exp(-1j * gate * alpha * theta)[..., None]
+    ub = np.exp(1j * gate * (1 - alpha) * theta)[..., None]
+    return (1 - alpha) * Fa * ua + alpha * Fb * ub
+
+
+def _blend_alpha_swapped(Fa, Fb, theta, gate, alpha):
+    ua = np.exp(1j * gate * alpha * theta)[..., None]
+    ub = np.exp(-1j * gate * (1 - alpha) * theta)[..., None]
+    return alpha * Fa * ua + (1 - alpha) * Fb * ub
+
+
+def _blend_drop_gate(Fa, Fb, theta, gate, alpha):
+    return P.blend(Fa, Fb, theta, np.ones_like(gate), alpha)
+
+
+def _dft_sign(n, sign):
+    k = np.arange(n)
+    return np.exp(-sign * 2j * np.pi * np.outer(k, k) / n)
+
+
+def _wrap_no_canon(z):
+    return math.atan2(z.imag, z.real)
+
+
+def _bin_tables_kappa1(hp, wp):
+    kind, partner, kappa, nu = P.bin_tables(hp, wp)
+    return kind, partner, np.ones_like(kappa), nu
+
+
+def _bin_tables_mirror_swap(hp, wp):
+    kind, partner, kappa, nu = P.bin_tables(hp, wp)
+    kind = kind.copy()
+    rep, mir = kind == P.REP, kind == P.MIRROR
+    self_col = np.zeros_like(rep)
+    self_col[:, 0] = True
+    if wp % 2 == 0:
+        self_col[:, wp // 2] = True
+    kind[rep & self_col] = P.MIRROR
+    kind[mir] = P.REP
+    return kind, partner, kappa, nu
+
+
+def _composition_clip(anchors, n):
+    return [(t, a, b, min(max(al, 0.0), 1.0)) for (t, a, b, al) in P.composition(anchors, n)]
+
+
+def _composition_wrong_pair(anchors, n):
+    a = list(anchors)
+    out = []
+    for (t, pa, pb, al) in P.composition(anchors, n):
+        if t > a[-1]:
+            pa, pb = a[0], a[1]
+            al = (t - pa) / (pb - pa)
+        out.append((t, pa, pb, al))
+    return out
+
+
+PAR_MUTANTS = {
+    "cross_no_conj": dict(cross_spectrum=_cross_no_conj),
+    "cross_swapped": dict(cross_spectrum=_cross_swapped),
+    "blend_sign": dict(blend=_blend_sign),
+    "blend_alpha_swapped": dict(blend=_blend_alpha_swapped),
+    "blend_drop_gate": dict(blend=_blend_drop_gate),
+    "dft_sign": dict(dft_matrix=_dft_sign),
+    "wrap_no_canon": dict(wrap_arg=_wrap_no_canon),
+    "kappa_all_one": dict(bin_tables=_bin_tables_kappa1),
+    "mirror_rep_swapped": dict(bin_tables=_bin_tables_mirror_swap),
+}
+
+
+def _any_pin_fails(mod, pins):
+    for pin in pins:
+        try:
+            pin(mod)
+        except AssertionError:
+            return pin.__name__
+    return None
+
+
+@pytest.mark.parametrize("name", sorted(PAR_MUTANTS))
+def test_par_mutation_caught(name):
+    mod = clone(P, **PAR_MUTANTS[name])
+    caught = _any_pin_fails(mod, TP.PINS)
+    assert caught, f"no PAR pin catches mutation {name}"
+
+
+def test_composition_mutations_caught():
+    cases = TP.load_composition_golden()
+    for fn in (_composition_clip, _composition_wrong_pair):
+        bad = False
+        for n, anchors, rows in cases:
+            got = fn(anchors, n)
+            if [(t, a, b, round(x, 12)) for t, a, b, x in got] != \
+                    [(t, a, b, round(x, 12)) for t, a, b, x in rows]:
+                bad = True
+        assert bad, fn.__name__
+
+
+def _key_sum_not_mean(q, k_hist):
+    return np.asarray(q, np.float64).mean(axis=1), np.asarray(k_hist, np.float64).sum(axis=1)
+
+
+def _topk_upper_tie(scores_1d, topk):
+    s = [float(x) for x in scores_1d]
+    order = sorted(range(len(s)), key=lambda m: (-s[m], -m))
+    return sorted(order[:min(topk, len(s))])
+
+
+def _topk_unsorted(scores_1d, topk):
+    s = [float(x) for x in scores_1d]
+    order = sorted(range(len(s)), key=lambda m: (-s[m], m))
+    return order[:min(topk, len(s))]
+
+
+def _attn_no_scale(Q, K, V, scale):
+    return A.softmax_attention(Q, K, V, 1.0)
+
+
+def _attn_transposed_v(Q, K, V, scale):
+    logits = scale * (Q @ K.T)
+    p = np.exp(logits - logits.max(1, keepdims=True))
+    p /= p.sum(1, keepdims=True)
+    out = np.zeros((Q.shape[0], V.shape[1]))
+    for r in range(Q.shape[0]):
+        out[r] = (p[r][:, None] * V[::-1]).sum(0)
+    return out, np.zeros(Q.shape[0])
+
+
+ROUTE_MUTANTS = {
+    "key_sum_not_mean": dict(pooled_means=_key_sum_not_mean),
+    "tie_upper_index": dict(topk_select=_topk_upper_tie),
+    "unsorted_output": dict(topk_select=_topk_unsorted),
+}
+ATTN_MUTANTS = {
+    "no_scale": dict(softmax_attention=_attn_no_scale),
+    "reversed_values": dict(softmax_attention=_attn_transposed_v),
+}
+
+
+@pytest.mark.parametrize("name", sorted(ROUTE_MUTANTS))
+def test_route_mutation_caught(name):
+    mod = clone(R, **ROUTE_MUTANTS[name])
+    assert _any_pin_fails(mod, TR.ROUTE_PINS), name
+
+
+@pytest.mark.parametrize("name", sorted(ATTN_MUTANTS))
+def test_attn_mutation_caught(name):
+    mod = clone(A, **ATTN_MUTANTS[name])
+    assert _any_pin_fails(mod, TR.ATTN_PINS), name
