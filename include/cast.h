@@ -1,0 +1,206 @@
+/*
+ * cast.h -- C ABI of libcast.so, the MI355X (gfx950) hot path of one
+ * reconstruction-coupled DiT block step of CAST ("CAST: Reconstruction-Coupled
+ * Acceleration of Interactive World Models").
+ *
+ * One block step at an eligible visual attention residual site is
+ *
+ *   cast_route_kv         pooled chunk scores and fixed-budget TopK over the
+ *                         historical KV blocks                 (Sec. 4.4 eq:pooled, eq:topk)
+ *   cast_anchor_attn      block-sparse attention of the anchor frames over the
+ *                         routed blocks (plus an optional always-available
+ *                         current/text segment)                 (Sec. 4.4, App. B.4)
+ *   cast_par_reconstruct  Phase-Aware Reconstruction of every skipped frame's
+ *                         residual from its two anchors         (Sec. 4.3 eq:cross,
+ *                         eq:confidence, eq:gate, eq:fcpasm; App. A.2; eq:block)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.    Tensor arguments are DEVICE pointers owned by the caller; the library
+ *            never allocates or frees device memory.  Scratch space is a caller-owned
+ *            device `workspace` sized by the matching *_workspace_bytes() query
+ *            (256-byte aligned).  `anchors` (PAR) is a small HOST array.
+ * Layout.    Token-major, channel-fastest, densely packed, matching a DiT hidden
+ *            state [frames, tokens, D] with D = H * dh head-major:
+ *              Q       bf16 [n_a, S, H, dh]      (anchor frames only)
+ *              K, V    bf16 [M, Bv, H, dh]       (M historical blocks of Bv tokens)
+ *              resid   fp32 [n_frames, Hg, Wg, D]
+ *            bf16 is IEEE binary32 truncated to its upper 16 bits (as torch.bfloat16).
+ * Streams.   Every call only enqueues work on `stream` (NULL = the legacy default
+ *            stream) and returns; nothing synchronises the host.  Asynchronous
+ *            device faults surface at the caller's next stream synchronisation.
+ * Errors.    Every call validates its arguments before enqueueing anything and
+ *            returns a cast_status_t; it never throws or aborts across the ABI.
+ *            cast_last_error_detail() gives a thread-local human-readable reason
+ *            for the last non-OK status of the calling thread.
+ * Threads.   Calls are re-entrant; the library holds no global mutable state other
+ *            than the thread-local error detail.
+ * Determinism. Results are bit-identical from run to run for identical inputs
+ *            (fixed-order reductions, no floating-point atomics).
+ */
+#ifndef CAST_H_
+#define CAST_H_
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CAST_ABI_VERSION 1
+
+typedef enum {
+  CAST_OK = 0,
+  CAST_ERR_NULL = 1,          /* a required pointer is NULL */
+  CAST_ERR_SHAPE = 2,         /* a size is out of range or inconsistent */
+  CAST_ERR_ANCHORS = 3,       /* anchors not strictly increasing in [0, n_frames), or K_f < 2 */
+  CAST_ERR_UNSUPPORTED = 4,   /* valid request outside what the kernels implement */
+  CAST_ERR_WORKSPACE = 5,     /* workspace NULL, misaligned or smaller than required */
+  CAST_ERR_HIP = 6            /* a HIP launch or runtime call failed */
+} cast_status_t;
+
+/* Static string naming a status value. */
+const char* cast_status_string(int status);
+
+/* Thread-local detail of the calling thread's most recent non-OK status
+ * (empty string if none).  Valid until the thread's next failing call. */
+const char* cast_last_error_detail(void);
+
+/* CAST_ABI_VERSION of the built library. */
+int cast_abi_version(void);
+
+/* ------------------------------------------------------------------------- */
+/* Routing (Sec. 4.4 eq:pooled; eq:topk; App. B.3 budget rules)              */
+/* ------------------------------------------------------------------------- */
+
+/* Device scratch (bytes) needed by cast_route_kv for these sizes. */
+size_t cast_route_kv_workspace_bytes(int n_a, int S, int H, int dh, int M, int Bv);
+
+/*
+ * Pooled chunk scores and TopK block selection, per (anchor frame i, head h):
+ *
+ *   q_bar[i,h,:] = mean over the S tokens of q[i,:,h,:]          (fp32 accumulation)
+ *   k_bar[m,h,:] = mean over the Bv tokens of k_hist[m,:,h,:]   (fp32 accumulation)
+ *   s[i,h,m]     = scale * dot(q_bar[i,h,:], k_bar[m,h,:])      (eq:pooled; the paper's
+ *                                                                scale is 1/sqrt(dh))
+ *   idx[i,h,:]   = the k_eff chunks with the largest s under the total order
+ *                  (score descending, chunk index ascending), written in
+ *                  ASCENDING chunk order; k_eff = min(topk, M) (App. B.3: with fewer
+ *                  than topk blocks all are kept and the realised budget reported).
+ *
+ * q        bf16 [n_a, S, H, dh] device.      k_hist  bf16 [M, Bv, H, dh] device.
+ * n_a>=1, S>=1, H>=1, dh in {32, 64, 128}, 0<=M<=4096, Bv>=1, topk>=1.
+ * scores_out  fp32 [n_a, H, M] device, or NULL to skip.
+ * idx_out     int32 [n_a, H, k_eff] device, densely packed (rows of k_eff entries,
+ *             the layout cast_anchor_attn takes).  May be NULL only when M == 0.
+ * k_eff_out   HOST int, receives k_eff (required).
+ * M == 0: k_eff = 0 and nothing is enqueued (routing bypassed, App. B.3).
+ * NaN scores give an unspecified but in-range selection.
+ */
+cast_status_t cast_route_kv(const void* q, const void* k_hist,
+                            int n_a, int S, int H, int dh, int M, int Bv,
+                            int topk, float scale,
+                            float* scores_out, int32_t* idx_out, int* k_eff_out,
+                            void* workspace, size_t workspace_bytes,
+                            hipStream_t stream);
+
+/* ------------------------------------------------------------------------- */
+/* Routed block-sparse anchor attention (Sec. 4.4; App. B.4 complexity)      */
+/* ------------------------------------------------------------------------- */
+
+/*
+ * For every anchor frame i and head h, with the key sequence
+ *     [ k_cur[0..n0) ; k_hist[idx[i,h,0]] ; ... ; k_hist[idx[i,h,k_eff-1]] ]
+ * of n0 + k_eff*Bv tokens (values likewise):
+ *     out[i,s,h,:] = softmax_j(scale * q[i,s,h,:] . key_j) value_j
+ * with fp32 logits, softmax and accumulation and bf16 output (the paper's BF16
+ * QKV / FP32 softmax precision, tab:config).
+ *
+ * q        bf16 [n_a, S, H, dh] device.   k_hist, v_hist bf16 [M, Bv, H, dh] device.
+ * idx      int32 [n_a, H, k_eff] device (as written by cast_route_kv); entries
+ *          outside [0, M) are clamped into it so no access leaves k_hist/v_hist.
+ * k_cur, v_cur  bf16 [n0, H, dh] device, the always-attended current/text segment;
+ *          may be NULL when n0 == 0.
+ * n0 >= 0, 0 <= k_eff <= M, n0 + k_eff*Bv >= 1; dh in {32, 64, 128};
+ * scale finite and > 0; (n0 + k_eff*Bv) * Bv < 2^40 and n0 + k_eff*Bv < 2^24 * Bv.
+ * out      bf16 [n_a, S, H, dh] device (must not alias the inputs).
+ * lse_out  fp32 [n_a, H, S] device natural-log sum of exp of the scaled logits,
+ *          or NULL to skip.
+ */
+cast_status_t cast_anchor_attn(const void* q, const void* k_hist, const void* v_hist,
+                               const int32_t* idx, int k_eff,
+                               const void* k_cur, const void* v_cur, int n0,
+                               int n_a, int S, int H, int dh, int M, int Bv,
+                               float scale, void* out, float* lse_out,
+                               hipStream_t stream);
+
+/* ------------------------------------------------------------------------- */
+/* Phase-Aware Reconstruction (Sec. 4.3; App. A.2; eq:block)                 */
+/* ------------------------------------------------------------------------- */
+
+typedef struct {
+  int tile_h, tile_w;          /* disjoint spatial tiles, 1..8 each; default 8 x 8
+                                  (tab:config_cast); edge tiles use their own size */
+  float tau_low, tau_high;     /* eq:gate frequency prior, default 0.25, 0.75 */
+  float q, T;                  /* eq:gate exponent and temperature, default 2, 0.10 */
+  float eta_rel, eta_abs;      /* reliability threshold eta = eta_rel*max W + eta_abs,
+                                  default 1e-6, 1e-8 (App. A.2) */
+  float eps;                   /* eq:confidence stabiliser, default 1e-8 */
+  int gate_mode;               /* 0: eq:gate; 1: g = 1 (full transport);
+                                  2: g = 0 (linear interpolation / extrapolation) */
+  int accumulate;              /* 0: out[t] = R_hat_t;  1: out[t] += R_hat_t, i.e.
+                                  X_t <- X_t + R~_t of eq:block */
+} cast_par_params_t;
+
+/* Fill *p with the paper's settings (tab:config_cast, App. A.2), write mode. */
+void cast_par_params_default(cast_par_params_t* p);
+
+/* Device scratch (bytes) needed by cast_par_reconstruct for these sizes. */
+size_t cast_par_workspace_bytes(int n_frames, int n_anchor, int Hg, int Wg, int D,
+                                const cast_par_params_t* params);
+
+/*
+ * Reconstruct the residual of every skipped frame t (t in [0, n_frames) not an
+ * anchor) from its anchor pair per eq:block: interior t uses the bracketing
+ * pair (a, b); t < a_0 uses (a_0, a_1); t > a_J uses (a_{J-1}, a_J);
+ * alpha = (t - a)/(b - a), never clipped.  Per pair (a, b) and tile p:
+ *   F = orthonormal 2-D real FFT of each channel of the tile (halved last axis),
+ *   Z = sum_c F_b conj(F_a),  W = sum_c |F_b||F_a|          (eq:cross, all D channels)
+ *   reliable: W > eta and |Z| > eta, eta = eta_rel * max_stored W + eta_abs;
+ *   theta = Arg Z in (-pi, pi] on reliable representative bins, -theta on their
+ *   mirrors, 0 on self-conjugate or unreliable bins;
+ *   c_p = sum_{reliable, non-DC} kappa |Z| / (sum kappa W + eps), 0 if none
+ *                                                        (eq:confidence);
+ *   g = sigmoid((c_p - tau_low - (tau_high - tau_low) nu^q) / T)   (eq:gate);
+ *   F_hat = (1-alpha) F_a e^{i g alpha theta} + alpha F_b e^{-i g (1-alpha) theta}
+ *                                                        (eq:fcpasm);
+ *   R_hat_t = inverse orthonormal real FFT, tiles assembled.
+ *
+ * resid    fp32 [n_frames, Hg, Wg, D] device; only the anchor frames are read.
+ * anchors  HOST int[n_anchor], strictly increasing in [0, n_frames); n_anchor >= 2
+ *          unless n_anchor == n_frames (K_f = N_cur: nothing to reconstruct, no
+ *          work enqueued, App. A.1).  n_frames <= 4096, n_anchor <= 512.
+ * out      fp32 [n_frames, Hg, Wg, D] device; only skipped-frame slots are
+ *          written (or accumulated into); anchor slots are never touched.  `out`
+ *          may be `resid` itself (write mode fills the skipped slots in place).
+ * theta_out, gate_out  fp32 [n_anchor-1, n_tiles, tile_h*(tile_w/2+1)] device or
+ *          NULL: per adjacent pair, tile and stored bin (ky*(tile_w/2+1)+kx) the
+ *          transport phase and gate; entries past a smaller edge tile's bins are 0.
+ *          n_tiles = ceil(Hg/tile_h) * ceil(Wg/tile_w), row-major.
+ * conf_out fp32 [n_anchor-1, n_tiles] device or NULL: c_p per pair and tile.
+ * Sizes: Hg, Wg >= 1; D >= 1; n_frames * Hg * Wg * D < 2^40.
+ */
+cast_status_t cast_par_reconstruct(const float* resid, const int* anchors, int n_anchor,
+                                   int n_frames, int Hg, int Wg, int D,
+                                   const cast_par_params_t* params, float* out,
+                                   float* theta_out, float* gate_out, float* conf_out,
+                                   void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CAST_H_ */

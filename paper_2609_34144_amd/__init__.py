@@ -1,0 +1,200 @@
+"""Python binding of libcast.so (the MI355X hot path of one CAST block step).
+
+Argument marshalling only: every step of routing, anchor attention and PAR runs in
+the library's HIP kernels.  Tensors are torch device tensors (torch supplies the
+memory and the current HIP stream); the functions carry the C ABI names and
+arguments of include/cast.h, plus small conveniences that allocate outputs and
+workspaces with torch.
+
+There is no fallback: if libcast.so is missing or fails to load, every call
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcast.so")
+
+CAST_OK = 0
+STATUS_NAMES = {0: "CAST_OK", 1: "CAST_ERR_NULL", 2: "CAST_ERR_SHAPE", 3: "CAST_ERR_ANCHORS",
+                4: "CAST_ERR_UNSUPPORTED", 5: "CAST_ERR_WORKSPACE", 6: "CAST_ERR_HIP"}
+
+EXPORTED = ["cast_status_string", "cast_last_error_detail", "cast_abi_version",
+            "cast_route_kv_workspace_bytes", "cast_route_kv", "cast_anchor_attn",
+            "cast_par_params_default", "cast_par_workspace_bytes", "cast_par_reconstruct"]
+
+
+class CastError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {detail}")
+        self.status = status
+        self.detail = detail
+
+
+class ParParams(ctypes.Structure):
+    """cast_par_params_t."""
+    _fields_ = [("tile_h", ctypes.c_int), ("tile_w", ctypes.c_int),
+                ("tau_low", ctypes.c_float), ("tau_high", ctypes.c_float),
+                ("q", ctypes.c_float), ("T", ctypes.c_float),
+                ("eta_rel", ctypes.c_float), ("eta_abs", ctypes.c_float),
+                ("eps", ctypes.c_float), ("gate_mode", ctypes.c_int),
+                ("accumulate", ctypes.c_int)]
+
+
+_lib = None
+_c = ctypes
+_vp, _i, _f, _sz = _c.c_void_p, _c.c_int, _c.c_float, _c.c_size_t
+
+
+def load(path: str = LIB_PATH):
+    """Load libcast.so (after torch, so the library binds to torch's HIP runtime)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    import torch  # noqa: F401  (loads the HIP runtime libcast.so must share)
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run python -m paper_2609_34144_amd.build")
+    lib = ctypes.CDLL(path, mode=ctypes.RTLD_LOCAL)
+    lib.cast_status_string.restype = _c.c_char_p
+    lib.cast_status_string.argtypes = [_i]
+    lib.cast_last_error_detail.restype = _c.c_char_p
+    lib.cast_last_error_detail.argtypes = []
+    lib.cast_abi_version.restype = _i
+    lib.cast_route_kv_workspace_bytes.restype = _sz
+    lib.cast_route_kv_workspace_bytes.argtypes = [_i] * 6
+    lib.cast_route_kv.restype = _i
+    lib.cast_route_kv.argtypes = [_vp, _vp, _i, _i, _i, _i, _i, _i, _i, _f, _vp, _vp,
+                                  _c.POINTER(_i), _vp, _sz, _vp]
+    lib.cast_anchor_attn.restype = _i
+    lib.cast_anchor_attn.argtypes = [_vp, _vp, _vp, _vp, _i, _vp, _vp, _i, _i, _i, _i, _i, _i,
+                                     _i, _f, _vp, _vp, _vp]
+    lib.cast_par_params_default.restype = None
+    lib.cast_par_params_default.argtypes = [_c.POINTER(ParParams)]
+    lib.cast_par_workspace_bytes.restype = _sz
+    lib.cast_par_workspace_bytes.argtypes = [_i, _i, _i, _i, _i, _c.POINTER(ParParams)]
+    lib.cast_par_reconstruct.restype = _i
+    lib.cast_par_reconstruct.argtypes = [_vp, _c.POINTER(_i), _i, _i, _i, _i, _i,
+                                         _c.POINTER(ParParams), _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+    _lib = lib
+    return lib
+
+
+def _check(st: int):
+    if st != CAST_OK:
+        raise CastError(st, _lib.cast_last_error_detail().decode())
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def _ws(nbytes: int, device, workspace):
+    import torch
+    if nbytes == 0:
+        return None, 0
+    if workspace is not None:
+        return workspace, workspace.numel() * workspace.element_size()
+    # torch's caching allocator returns >= 512-byte aligned blocks
+    return torch.empty(nbytes, dtype=torch.uint8, device=device), nbytes
+
+
+# ---------------------------------------------------------------------------
+# C ABI mirrors
+# ---------------------------------------------------------------------------
+
+def cast_abi_version() -> int:
+    return load().cast_abi_version()
+
+
+def cast_route_kv_workspace_bytes(n_a, S, H, dh, M, Bv) -> int:
+    return load().cast_route_kv_workspace_bytes(n_a, S, H, dh, M, Bv)
+
+
+def cast_par_workspace_bytes(n_frames, n_anchor, Hg, Wg, D, params: ParParams) -> int:
+    return load().cast_par_workspace_bytes(n_frames, n_anchor, Hg, Wg, D, ctypes.byref(params))
+
+
+def cast_par_params_default(**overrides) -> ParParams:
+    p = ParParams()
+    load().cast_par_params_default(ctypes.byref(p))
+    for k, v in overrides.items():
+        setattr(p, k, v)
+    return p
+
+
+def cast_route_kv(q, k_hist, topk: int, scale: float = 1.0, scores_out=None, idx_out=None,
+                  workspace=None, stream=None, want_scores: bool = False):
+    """q bf16 [n_a, S, H, dh], k_hist bf16 [M, Bv, H, dh] (device).
+    Returns (idx int32 [n_a, H, k_eff], k_eff, scores fp32 [n_a, H, M] or None)."""
+    import torch
+    lib = load()
+    n_a, S, H, dh = q.shape
+    M, Bv = k_hist.shape[0], k_hist.shape[1]
+    k_eff_guess = min(topk, M)
+    if idx_out is None and M > 0:
+        idx_out = torch.empty((n_a, H, k_eff_guess), dtype=torch.int32, device=q.device)
+    if scores_out is None and want_scores and M > 0:
+        scores_out = torch.empty((n_a, H, M), dtype=torch.float32, device=q.device)
+    ws, wsb = _ws(lib.cast_route_kv_workspace_bytes(n_a, S, H, dh, M, Bv), q.device, workspace)
+    k_eff = ctypes.c_int(-1)
+    _check(lib.cast_route_kv(_ptr(q), _ptr(k_hist), n_a, S, H, dh, M, Bv, topk, scale,
+                             _ptr(scores_out), _ptr(idx_out), ctypes.byref(k_eff), _ptr(ws), wsb,
+                             _stream(stream)))
+    return idx_out, k_eff.value, scores_out
+
+
+def cast_anchor_attn(q, k_hist, v_hist, idx, k_eff: int, scale: float, k_cur=None, v_cur=None,
+                     out=None, lse_out=None, want_lse: bool = False, stream=None):
+    """Routed block-sparse attention of the anchor frames; returns (out bf16, lse or None)."""
+    import torch
+    lib = load()
+    n_a, S, H, dh = q.shape
+    M, Bv = k_hist.shape[0], k_hist.shape[1]
+    n0 = 0 if k_cur is None else k_cur.shape[0]
+    if out is None:
+        out = torch.empty_like(q)
+    if lse_out is None and want_lse:
+        lse_out = torch.empty((n_a, H, S), dtype=torch.float32, device=q.device)
+    _check(lib.cast_anchor_attn(_ptr(q), _ptr(k_hist), _ptr(v_hist), _ptr(idx), k_eff,
+                                _ptr(k_cur), _ptr(v_cur), n0, n_a, S, H, dh, M, Bv, scale,
+                                _ptr(out), _ptr(lse_out), _stream(stream)))
+    return out, lse_out
+
+
+def cast_par_reconstruct(resid, anchors, params: ParParams | None = None, out=None,
+                         theta_out=None, gate_out=None, conf_out=None, workspace=None,
+                         stream=None):
+    """PAR over resid fp32 [n_frames, Hg, Wg, D] (device) with host `anchors`.
+    Writes (or accumulates into) the skipped-frame slots of `out` (default: a new
+    zero tensor) and returns it."""
+    import torch
+    lib = load()
+    if params is None:
+        params = cast_par_params_default()
+    n_frames, Hg, Wg, D = resid.shape
+    anc = [int(a) for a in anchors]
+    arr = (ctypes.c_int * max(len(anc), 1))(*anc)
+    if out is None:
+        out = torch.zeros_like(resid)
+    nbytes = lib.cast_par_workspace_bytes(n_frames, len(anc), Hg, Wg, D, ctypes.byref(params))
+    ws, wsb = _ws(nbytes, resid.device, workspace)
+    _check(lib.cast_par_reconstruct(_ptr(resid), arr, len(anc), n_frames, Hg, Wg, D,
+                                    ctypes.byref(params), _ptr(out), _ptr(theta_out),
+                                    _ptr(gate_out), _ptr(conf_out), _ptr(ws), wsb,
+                                    _stream(stream)))
+    return out
+
+
+def par_debug_shapes(n_anchor, Hg, Wg, params: ParParams):
+    """Shapes of the optional theta/gate ([pairs, tiles, bins]) and conf ([pairs, tiles])."""
+    nt = -(-Hg // params.tile_h) * -(-Wg // params.tile_w)
+    return (n_anchor - 1, nt, params.tile_h * (params.tile_w // 2 + 1)), (n_anchor - 1, nt)

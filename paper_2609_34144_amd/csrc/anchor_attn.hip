@@ -1,0 +1,326 @@
+// Routed block-sparse anchor attention on gfx950 (Sec. 4.4; App. B.4).
+//
+// Flash-style single pass with bf16 MFMA (v_mfma_f32_32x32x16_bf16) and fp32
+// online softmax.  One workgroup = 4 waves = 128 queries of one (anchor, head);
+// each wave owns 32 queries.  The key sequence of the (anchor, head) is the
+// concatenation [current segment (n0 tokens) ; routed chunk idx[0] ; ... ], walked
+// in tiles of 64 keys; each tile's rows are gathered from their chunk by index
+// into LDS (double-buffered, one barrier per tile).
+//
+// Layout choices (per wave, per 64-key tile):
+//   S^T = K Q^T   A = K tile from LDS (row-major, padded rows), B = Q^T held in
+//                 registers for the whole kernel.  The 32x32 accumulator puts one
+//                 query per lane column, so the row max / row sum of the online
+//                 softmax need only the lane's own values and one exchange with
+//                 lane^32.
+//   O^T += V^T P^T  B = P^T straight from the S^T accumulators (converted to
+//                 bf16; the contraction index order is free, so no data moves),
+//                 A = V^T from an LDS copy of the V tile stored as
+//                 [key/4][d][key%4] so each lane reads its 4-key runs as 8 bytes.
+// Blocks are renumbered so that the Q-tiles of one (anchor, head) land on the
+// same XCD and share its L2 for the routed K/V.
+#include "cast_common.h"
+
+namespace cast {
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kBQ = 128;   // queries per workgroup
+constexpr int kBK = 64;    // keys per tile
+constexpr int kThreads = 256;
+
+struct AttnArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const int32_t* idx;
+  const uint16_t* kc;
+  const uint16_t* vc;
+  uint16_t* out;
+  float* lse;
+  int n_a, S, H, M, Bv, n0, k_eff, L, n_qt, nblocks;
+  unsigned long long bv_magic;   // ceil(2^40 / Bv): row / Bv = (row * magic) >> 40
+  float sl2;                     // scale * log2(e)
+};
+
+// Block b runs on XCD b % 8; give each XCD a contiguous range of logical blocks.
+__device__ __forceinline__ int xcd_remap(int b, int nb) {
+  const int per = nb / 8, rem = nb % 8;
+  const int xcd = b % 8, j = b / 8;
+  return (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + j;
+}
+
+template <int DH>
+__device__ __forceinline__ const uint16_t* row_ptr(const AttnArgs& a, const uint16_t* hist,
+                                                   const uint16_t* cur, const int32_t* idx_ih,
+                                                   int r, int h) {
+  if (r < a.n0) return cur + ((long long)r * a.H + h) * DH;
+  const unsigned rr = (unsigned)(r - a.n0);
+  const unsigned slot = (unsigned)(((unsigned long long)rr * a.bv_magic) >> 40);
+  const unsigned t = rr - slot * (unsigned)a.Bv;
+  int c = idx_ih[slot];
+  c = c < 0 ? 0 : (c >= a.M ? a.M - 1 : c);
+  return hist + (((long long)c * a.Bv + t) * a.H + h) * DH;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  // round to nearest even (finite inputs)
+  uint32_t a = __float_as_uint(lo), b = __float_as_uint(hi);
+  a += 0x7fffu + ((a >> 16) & 1u);
+  b += 0x7fffu + ((b >> 16) & 1u);
+  return (a >> 16) | (b & 0xffff0000u);
+}
+
+template <int DH>
+struct Tile {
+  static constexpr int KSTR = DH + 8;                // padded K row (bf16 elements)
+  static constexpr int K_ELEMS = kBK * KSTR;
+  static constexpr int V_ELEMS = kBK * DH;           // [kBK/4][DH][4]
+  static constexpr int CPR = DH / 8;                 // 16-byte chunks per row
+  static constexpr int RPP = kThreads / CPR;         // rows per load pass
+  static constexpr int KPASS = kBK / RPP;            // K load passes per tile
+  static constexpr int VITEMS = (kBK / 4) * CPR;     // V items (4 rows x 16 bytes)
+  static constexpr int VPASS = (VITEMS + kThreads - 1) / kThreads;
+};
+
+template <int DH>
+__global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
+  using T = Tile<DH>;
+  __shared__ __attribute__((aligned(16))) uint16_t lds_k[2][T::K_ELEMS];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_v[2][T::V_ELEMS];
+
+  const int logical = xcd_remap(blockIdx.x, a.nblocks);
+  const int pair = logical / a.n_qt, qt = logical - pair * a.n_qt;
+  const int i = pair / a.H, h = pair - (pair / a.H) * a.H;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int l32 = lane & 31, hf = lane >> 5;
+  const int32_t* idx_ih = a.idx ? a.idx + ((long long)i * a.H + h) * a.k_eff : nullptr;
+
+  // ---- Q^T operand in registers: lane holds query l32, d = 16t + 8hf .. +8
+  const int qi = qt * kBQ + wave * 32 + l32;
+  bf16x8 qreg[DH / 16];
+  {
+    const bool ok = qi < a.S;
+    const uint16_t* qp = a.q + (((long long)i * a.S + (ok ? qi : 0)) * a.H + h) * DH + 8 * hf;
+#pragma unroll
+    for (int t = 0; t < DH / 16; ++t) {
+      uint4 v = ok ? *reinterpret_cast<const uint4*>(qp + 16 * t) : make_uint4(0, 0, 0, 0);
+      qreg[t] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+
+  // ---- tile loaders (global -> registers -> LDS)
+  uint4 kbuf[T::KPASS];
+  uint4 vbuf[T::VPASS][4];
+  auto load_tile = [&](int tile) {
+    const int r0 = tile * kBK;
+#pragma unroll
+    for (int p = 0; p < T::KPASS; ++p) {
+      const int r = r0 + p * T::RPP + tid / T::CPR;
+      kbuf[p] = make_uint4(0, 0, 0, 0);
+      if (r < a.L) {
+        const uint16_t* src = row_ptr<DH>(a, a.k, a.kc, idx_ih, r, h);
+        kbuf[p] = *reinterpret_cast<const uint4*>(src + (tid % T::CPR) * 8);
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < T::VPASS; ++p) {
+      const int it = tid + p * kThreads;
+      const int g = it / T::CPR, ch = it % T::CPR;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const int r = r0 + 4 * g + kk;
+        vbuf[p][kk] = make_uint4(0, 0, 0, 0);
+        if (it < T::VITEMS && r < a.L) {
+          const uint16_t* src = row_ptr<DH>(a, a.v, a.vc, idx_ih, r, h);
+          vbuf[p][kk] = *reinterpret_cast<const uint4*>(src + ch * 8);
+        }
+      }
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int p = 0; p < T::KPASS; ++p) {
+      const int row = p * T::RPP + tid / T::CPR;
+      *reinterpret_cast<uint4*>(&lds_k[buf][row * T::KSTR + (tid % T::CPR) * 8]) = kbuf[p];
+    }
+#pragma unroll
+    for (int p = 0; p < T::VPASS; ++p) {
+      const int it = tid + p * kThreads;
+      if (it < T::VITEMS) {
+        const int g = it / T::CPR, ch = it % T::CPR;
+        const uint32_t* v0 = reinterpret_cast<const uint32_t*>(&vbuf[p][0]);
+        const uint32_t* v1 = reinterpret_cast<const uint32_t*>(&vbuf[p][1]);
+        const uint32_t* v2 = reinterpret_cast<const uint32_t*>(&vbuf[p][2]);
+        const uint32_t* v3 = reinterpret_cast<const uint32_t*>(&vbuf[p][3]);
+        uint4* dst = reinterpret_cast<uint4*>(&lds_v[buf][(g * DH + ch * 8) * 4]);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          // d = 8ch + 2w (low halves) and d = 8ch + 2w + 1 (high halves), keys 4g..4g+3
+          dst[w] = make_uint4(__builtin_amdgcn_perm(v1[w], v0[w], 0x05040100u),
+                              __builtin_amdgcn_perm(v3[w], v2[w], 0x05040100u),
+                              __builtin_amdgcn_perm(v1[w], v0[w], 0x07060302u),
+                              __builtin_amdgcn_perm(v3[w], v2[w], 0x07060302u));
+        }
+      }
+    }
+  };
+
+  f32x16 acc_o[DH / 32];
+#pragma unroll
+  for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc_o[db][e] = 0.0f;
+  float m_run = -INFINITY, l_run = 0.0f;
+
+  const int ntiles = (a.L + kBK - 1) / kBK;
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+
+  for (int tile = 0; tile < ntiles; ++tile) {
+    const int buf = tile & 1;
+    if (tile + 1 < ntiles) load_tile(tile + 1);
+
+    // ---- S^T = K Q^T for the 64 keys of this tile (two 32-key blocks)
+    f32x16 acc_s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc_s[kb][e] = 0.0f;
+      const uint16_t* kr = &lds_k[buf][(kb * 32 + l32) * T::KSTR + 8 * hf];
+#pragma unroll
+      for (int t = 0; t < DH / 16; ++t) {
+        bf16x8 ka = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kr + 16 * t));
+        acc_s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[t], acc_s[kb], 0, 0, 0);
+      }
+    }
+    // mask keys past the end of the sequence (last tile only)
+    const int key0 = tile * kBK;
+    if (key0 + kBK > a.L) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = key0 + kb * 32 + 8 * (e / 4) + 4 * hf + (e % 4);
+          if (key >= a.L) acc_s[kb][e] = -INFINITY;
+        }
+    }
+    // ---- online softmax (log2 domain)
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc_s[kb][e]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx * a.sl2);
+    const float corr = exp2f(m_run - m_new);
+    float rs = 0.0f;
+    bf16x8 pb[2][2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      float p[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        p[e] = exp2f(fmaf(acc_s[kb][e], a.sl2, -m_new));
+        rs += p[e];
+      }
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        uint4 w = make_uint4(pack_bf16x2(p[8 * s + 0], p[8 * s + 1]), pack_bf16x2(p[8 * s + 2], p[8 * s + 3]),
+                             pack_bf16x2(p[8 * s + 4], p[8 * s + 5]), pack_bf16x2(p[8 * s + 6], p[8 * s + 7]));
+        pb[kb][s] = __builtin_bit_cast(bf16x8, w);
+      }
+    }
+    l_run = l_run * corr + rs;
+    m_run = m_new;
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc_o[db][e] *= corr;
+
+    // ---- O^T += V^T P^T
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db) {
+      const int d = db * 32 + l32;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+          const int g = 8 * kb + 4 * s + hf;      // keys 4g..4g+3, then 4(g+2)..+3
+          const uint2 lo = *reinterpret_cast<const uint2*>(&lds_v[buf][(g * DH + d) * 4]);
+          const uint2 hi = *reinterpret_cast<const uint2*>(&lds_v[buf][((g + 2) * DH + d) * 4]);
+          bf16x8 va = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+          acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kb][s], acc_o[db], 0, 0, 0);
+        }
+    }
+
+    if (tile + 1 < ntiles) store_tile(buf ^ 1);
+    __syncthreads();
+  }
+
+  // ---- epilogue: normalise, write O (bf16) and the log-sum-exp
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float inv = 1.0f / l_tot;
+  if (qi < a.S) {
+    uint16_t* op = a.out + (((long long)i * a.S + qi) * a.H + h) * DH + 4 * hf;
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const uint2 w = make_uint2(pack_bf16x2(acc_o[db][4 * g4 + 0] * inv, acc_o[db][4 * g4 + 1] * inv),
+                                   pack_bf16x2(acc_o[db][4 * g4 + 2] * inv, acc_o[db][4 * g4 + 3] * inv));
+        *reinterpret_cast<uint2*>(op + db * 32 + 8 * g4) = w;
+      }
+    if (a.lse && hf == 0)
+      a.lse[((long long)i * a.H + h) * a.S + qi] = m_run * 0.69314718055994531f + logf(l_tot);
+  }
+}
+
+template <int DH>
+cast_status_t launch_dh(const AttnArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(anchor_attn_kernel<DH>, dim3(a.nblocks), dim3(kThreads), 0, stream, a);
+  return check_launch("anchor_attn");
+}
+
+}  // namespace
+
+cast_status_t launch_anchor_attn(const void* q, const void* k_hist, const void* v_hist,
+                                 const int32_t* idx, int k_eff, const void* k_cur,
+                                 const void* v_cur, int n0, int n_a, int S, int H, int dh, int M,
+                                 int Bv, float scale, void* out, float* lse_out,
+                                 hipStream_t stream) {
+  AttnArgs a{};
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k_hist);
+  a.v = static_cast<const uint16_t*>(v_hist);
+  a.idx = k_eff > 0 ? idx : nullptr;
+  a.kc = static_cast<const uint16_t*>(k_cur);
+  a.vc = static_cast<const uint16_t*>(v_cur);
+  a.out = static_cast<uint16_t*>(out);
+  a.lse = lse_out;
+  a.n_a = n_a;
+  a.S = S;
+  a.H = H;
+  a.M = M;
+  a.Bv = Bv;
+  a.n0 = n0;
+  a.k_eff = k_eff;
+  a.L = n0 + k_eff * Bv;
+  a.n_qt = (S + kBQ - 1) / kBQ;
+  a.nblocks = n_a * H * a.n_qt;
+  a.bv_magic = ((1ull << 40) + (unsigned long long)Bv - 1) / (unsigned long long)Bv;
+  a.sl2 = scale * 1.4426950408889634f;
+  switch (dh) {
+    case 32: return launch_dh<32>(a, stream);
+    case 64: return launch_dh<64>(a, stream);
+    case 128: return launch_dh<128>(a, stream);
+    default: return fail(CAST_ERR_UNSUPPORTED, "attn: dh %d", dh);
+  }
+}
+
+}  // namespace cast

@@ -1,0 +1,207 @@
+// C ABI entry points of libcast: argument validation, workspace sizing and
+// dispatch to the kernel launchers.  Every entry point validates all of its
+// arguments before anything is enqueued and reports failures as a status plus
+// a thread-local detail string.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "cast_common.h"
+
+namespace cast {
+
+static thread_local char g_detail[512] = "";
+
+cast_status_t fail(cast_status_t st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_detail, sizeof(g_detail), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+cast_status_t check_launch(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(CAST_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return CAST_OK;
+}
+
+static bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+static cast_status_t check_ws(void* ws, size_t have, size_t need) {
+  if (need == 0) return CAST_OK;
+  if (ws == nullptr) return fail(CAST_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", need);
+  if (!aligned(ws, kWsAlign)) return fail(CAST_ERR_WORKSPACE, "workspace must be %zu-byte aligned", kWsAlign);
+  if (have < need) return fail(CAST_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", have, need);
+  return CAST_OK;
+}
+
+static bool dh_ok(int dh) { return dh == 32 || dh == 64 || dh == 128; }
+
+}  // namespace cast
+
+using namespace cast;
+
+extern "C" {
+
+const char* cast_status_string(int s) {
+  switch (s) {
+    case CAST_OK: return "CAST_OK";
+    case CAST_ERR_NULL: return "CAST_ERR_NULL";
+    case CAST_ERR_SHAPE: return "CAST_ERR_SHAPE";
+    case CAST_ERR_ANCHORS: return "CAST_ERR_ANCHORS";
+    case CAST_ERR_UNSUPPORTED: return "CAST_ERR_UNSUPPORTED";
+    case CAST_ERR_WORKSPACE: return "CAST_ERR_WORKSPACE";
+    case CAST_ERR_HIP: return "CAST_ERR_HIP";
+    default: return "CAST_ERR_UNKNOWN";
+  }
+}
+
+const char* cast_last_error_detail(void) { return g_detail; }
+
+int cast_abi_version(void) { return CAST_ABI_VERSION; }
+
+// ------------------------------------------------------------------ routing
+
+static cast_status_t route_shape_check(int n_a, int S, int H, int dh, int M, int Bv) {
+  if (n_a < 1 || S < 1 || H < 1 || M < 0 || Bv < 1)
+    return fail(CAST_ERR_SHAPE, "route: need n_a>=1, S>=1, H>=1, M>=0, Bv>=1 (got %d %d %d %d %d)",
+                n_a, S, H, M, Bv);
+  if (!dh_ok(dh)) return fail(CAST_ERR_UNSUPPORTED, "route: dh must be 32, 64 or 128 (got %d)", dh);
+  if (M > kRouteMaxM) return fail(CAST_ERR_UNSUPPORTED, "route: M=%d exceeds %d chunks", M, kRouteMaxM);
+  if ((long long)S * H * dh >= (1LL << 31) || (long long)Bv * H * dh >= (1LL << 31))
+    return fail(CAST_ERR_UNSUPPORTED, "route: one frame or chunk must hold < 2^31 elements");
+  if ((long long)M * Bv >= (1LL << 31) || (long long)n_a * S >= (1LL << 31))
+    return fail(CAST_ERR_UNSUPPORTED, "route: token counts must stay below 2^31");
+  return CAST_OK;
+}
+
+size_t cast_route_kv_workspace_bytes(int n_a, int S, int H, int dh, int M, int Bv) {
+  if (route_shape_check(n_a, S, H, dh, M, Bv) != CAST_OK || M == 0) return 0;
+  return plan_route(n_a, S, H, dh, M, Bv).total;
+}
+
+cast_status_t cast_route_kv(const void* q, const void* k_hist, int n_a, int S, int H, int dh,
+                            int M, int Bv, int topk, float scale, float* scores_out,
+                            int32_t* idx_out, int* k_eff_out, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream) {
+  if (k_eff_out == nullptr) return fail(CAST_ERR_NULL, "route: k_eff_out is NULL");
+  cast_status_t st = route_shape_check(n_a, S, H, dh, M, Bv);
+  if (st != CAST_OK) return st;
+  if (topk < 1) return fail(CAST_ERR_SHAPE, "route: topk must be >= 1 (got %d)", topk);
+  if (M == 0) { *k_eff_out = 0; return CAST_OK; }          // routing bypassed (App. B.3)
+  if (q == nullptr || k_hist == nullptr || idx_out == nullptr)
+    return fail(CAST_ERR_NULL, "route: q, k_hist and idx_out are required");
+  if (!aligned(q, 16) || !aligned(k_hist, 16))
+    return fail(CAST_ERR_SHAPE, "route: q and k_hist must be 16-byte aligned");
+  RoutePlan plan = plan_route(n_a, S, H, dh, M, Bv);
+  st = check_ws(workspace, workspace_bytes, plan.total);
+  if (st != CAST_OK) return st;
+  int k_eff = topk < M ? topk : M;
+  st = launch_route(q, k_hist, n_a, S, H, dh, M, Bv, k_eff, scale, scores_out, idx_out, plan,
+                    workspace, stream);
+  if (st != CAST_OK) return st;
+  *k_eff_out = k_eff;
+  return CAST_OK;
+}
+
+// ---------------------------------------------------------------- attention
+
+cast_status_t cast_anchor_attn(const void* q, const void* k_hist, const void* v_hist,
+                               const int32_t* idx, int k_eff, const void* k_cur,
+                               const void* v_cur, int n0, int n_a, int S, int H, int dh, int M,
+                               int Bv, float scale, void* out, float* lse_out,
+                               hipStream_t stream) {
+  if (n_a < 1 || S < 1 || H < 1 || M < 0 || Bv < 1 || n0 < 0 || k_eff < 0)
+    return fail(CAST_ERR_SHAPE, "attn: need n_a,S,H,Bv>=1 and M,n0,k_eff>=0");
+  if (!dh_ok(dh)) return fail(CAST_ERR_UNSUPPORTED, "attn: dh must be 32, 64 or 128 (got %d)", dh);
+  if (k_eff > M) return fail(CAST_ERR_SHAPE, "attn: k_eff=%d exceeds M=%d", k_eff, M);
+  long long L = (long long)n0 + (long long)k_eff * Bv;
+  if (L < 1) return fail(CAST_ERR_SHAPE, "attn: nothing to attend to (n0 = 0 and k_eff = 0)");
+  if (L * (long long)Bv >= (1LL << 40) || L >= (1LL << 31) || L >= (1LL << 24) * (long long)Bv)
+    return fail(CAST_ERR_UNSUPPORTED, "attn: key sequence too long for the row indexing");
+  if (!(scale > 0.0f) || scale > 3.0e38f)
+    return fail(CAST_ERR_SHAPE, "attn: scale must be finite and > 0");
+  if ((long long)M * Bv >= (1LL << 31) || (long long)n_a * S >= (1LL << 31))
+    return fail(CAST_ERR_UNSUPPORTED, "attn: token counts must stay below 2^31");
+  if (q == nullptr || out == nullptr) return fail(CAST_ERR_NULL, "attn: q and out are required");
+  if (k_eff > 0 && (k_hist == nullptr || v_hist == nullptr || idx == nullptr))
+    return fail(CAST_ERR_NULL, "attn: k_hist, v_hist and idx are required when k_eff > 0");
+  if (n0 > 0 && (k_cur == nullptr || v_cur == nullptr))
+    return fail(CAST_ERR_NULL, "attn: k_cur and v_cur are required when n0 > 0");
+  const void* ptrs[] = {q, k_hist, v_hist, k_cur, v_cur, out};
+  for (const void* p : ptrs)
+    if (p != nullptr && !aligned(p, 16)) return fail(CAST_ERR_SHAPE, "attn: tensors must be 16-byte aligned");
+  return launch_anchor_attn(q, k_hist, v_hist, idx, k_eff, k_cur, v_cur, n0, n_a, S, H, dh, M,
+                            Bv, scale, out, lse_out, stream);
+}
+
+// ---------------------------------------------------------------------- PAR
+
+void cast_par_params_default(cast_par_params_t* p) {
+  if (p == nullptr) return;
+  p->tile_h = 8;
+  p->tile_w = 8;
+  p->tau_low = 0.25f;
+  p->tau_high = 0.75f;
+  p->q = 2.0f;
+  p->T = 0.10f;
+  p->eta_rel = 1e-6f;
+  p->eta_abs = 1e-8f;
+  p->eps = 1e-8f;
+  p->gate_mode = 0;
+  p->accumulate = 0;
+}
+
+static cast_status_t par_shape_check(int n_frames, int n_anchor, int Hg, int Wg, int D,
+                                     const cast_par_params_t* p) {
+  if (p == nullptr) return fail(CAST_ERR_NULL, "par: params is NULL");
+  if (n_frames < 1 || Hg < 1 || Wg < 1 || D < 1 || n_anchor < 1)
+    return fail(CAST_ERR_SHAPE, "par: need n_frames, n_anchor, Hg, Wg, D >= 1");
+  if (n_frames > kParMaxFrames) return fail(CAST_ERR_UNSUPPORTED, "par: n_frames > %d", kParMaxFrames);
+  if (n_anchor > kParMaxAnchors) return fail(CAST_ERR_UNSUPPORTED, "par: n_anchor > %d", kParMaxAnchors);
+  if (n_anchor > n_frames) return fail(CAST_ERR_ANCHORS, "par: more anchors than frames");
+  if (p->tile_h < 1 || p->tile_h > kParMaxTile || p->tile_w < 1 || p->tile_w > kParMaxTile)
+    return fail(CAST_ERR_UNSUPPORTED, "par: tile edges must be in [1, %d]", kParMaxTile);
+  if (p->gate_mode < 0 || p->gate_mode > 2) return fail(CAST_ERR_SHAPE, "par: gate_mode must be 0, 1 or 2");
+  if (!(p->T > 0.0f) || !(p->q > 0.0f) || !(p->tau_high >= p->tau_low))
+    return fail(CAST_ERR_SHAPE, "par: eq:gate needs q > 0, T > 0, tau_high >= tau_low");
+  if ((long long)Hg * Wg * D >= (1LL << 31))
+    return fail(CAST_ERR_UNSUPPORTED, "par: one frame must hold < 2^31 elements");
+  return CAST_OK;
+}
+
+size_t cast_par_workspace_bytes(int n_frames, int n_anchor, int Hg, int Wg, int D,
+                                const cast_par_params_t* params) {
+  if (par_shape_check(n_frames, n_anchor, Hg, Wg, D, params) != CAST_OK) return 0;
+  if (n_anchor == n_frames || n_anchor < 2) return 0;
+  return plan_par(n_frames, n_anchor, Hg, Wg, D, *params).total;
+}
+
+cast_status_t cast_par_reconstruct(const float* resid, const int* anchors, int n_anchor,
+                                   int n_frames, int Hg, int Wg, int D,
+                                   const cast_par_params_t* params, float* out,
+                                   float* theta_out, float* gate_out, float* conf_out,
+                                   void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream) {
+  if (anchors == nullptr) return fail(CAST_ERR_NULL, "par: anchors is NULL");
+  cast_status_t st = par_shape_check(n_frames, n_anchor, Hg, Wg, D, params);
+  if (st != CAST_OK) return st;
+  for (int j = 0; j < n_anchor; ++j) {
+    if (anchors[j] < 0 || anchors[j] >= n_frames)
+      return fail(CAST_ERR_ANCHORS, "par: anchor %d = %d outside [0, %d)", j, anchors[j], n_frames);
+    if (j > 0 && anchors[j] <= anchors[j - 1])
+      return fail(CAST_ERR_ANCHORS, "par: anchors must be strictly increasing (index %d)", j);
+  }
+  if (n_anchor == n_frames) return CAST_OK;                 // K_f = N_cur: bypass (App. A.1)
+  if (n_anchor < 2) return fail(CAST_ERR_ANCHORS, "par: reconstruction needs K_f >= 2 anchors");
+  if (resid == nullptr || out == nullptr) return fail(CAST_ERR_NULL, "par: resid and out are required");
+  if (!aligned(resid, 4) || !aligned(out, 4)) return fail(CAST_ERR_SHAPE, "par: misaligned buffers");
+  ParPlan plan = plan_par(n_frames, n_anchor, Hg, Wg, D, *params);
+  st = check_ws(workspace, workspace_bytes, plan.total);
+  if (st != CAST_OK) return st;
+  return launch_par(resid, anchors, n_anchor, n_frames, Hg, Wg, D, *params, out, theta_out,
+                    gate_out, conf_out, plan, workspace, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,81 @@
+// Internal declarations shared by the libcast translation units (not installed).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/cast.h"
+
+namespace cast {
+
+// ---------------------------------------------------------------------------
+// Error reporting (thread-local detail string, see cast_last_error_detail)
+// ---------------------------------------------------------------------------
+cast_status_t fail(cast_status_t st, const char* fmt, ...);
+cast_status_t check_launch(const char* what);
+
+constexpr size_t kWsAlign = 256;
+inline size_t align_up(size_t x, size_t a = kWsAlign) { return (x + a - 1) / a * a; }
+
+// ---------------------------------------------------------------------------
+// bf16 <-> fp32 on the device (bf16 = upper half of binary32)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// ---------------------------------------------------------------------------
+// Routing plan: how the pooled-mean scan is split (shared by the workspace
+// query and the launch so both agree).
+// ---------------------------------------------------------------------------
+struct RoutePlan {
+  int D;            // H * dh
+  int ngrp;         // channel groups of kPoolChannels
+  int spq, tq;      // splits per anchor frame, tokens per split
+  int spk, tk;      // splits per history chunk, tokens per split
+  int items;        // n_a * spq + M * spk
+  size_t off_partial, off_means, off_scores, total;
+};
+constexpr int kPoolThreads = 64;
+constexpr int kPoolChannels = kPoolThreads * 8;   // 8 bf16 channels per thread
+constexpr int kRouteMaxM = 4096;   // bitonic keys live in 32 KB of LDS
+
+RoutePlan plan_route(int n_a, int S, int H, int dh, int M, int Bv);
+
+cast_status_t launch_route(const void* q, const void* k, int n_a, int S, int H, int dh, int M,
+                           int Bv, int k_eff, float scale, float* scores_out, int32_t* idx_out,
+                           const RoutePlan& plan, void* ws, hipStream_t stream);
+
+// ---------------------------------------------------------------------------
+// Attention
+// ---------------------------------------------------------------------------
+cast_status_t launch_anchor_attn(const void* q, const void* k_hist, const void* v_hist,
+                                 const int32_t* idx, int k_eff, const void* k_cur,
+                                 const void* v_cur, int n0, int n_a, int S, int H, int dh, int M,
+                                 int Bv, float scale, void* out, float* lse_out,
+                                 hipStream_t stream);
+
+// ---------------------------------------------------------------------------
+// PAR
+// ---------------------------------------------------------------------------
+constexpr int kParMaxTile = 8;
+constexpr int kParMaxAnchors = 512;
+constexpr int kParMaxFrames = 4096;
+constexpr int kParNkxMax = kParMaxTile / 2 + 1;           // 5 stored columns
+constexpr int kParBinsMax = kParMaxTile * kParNkxMax;     // 40 stored bins
+
+struct ParPlan {
+  int n_pairs, n_tiles, n_tiles_y, n_tiles_x;
+  int chb;              // channels per xspec block
+  int n_chblk;          // channel blocks for the cross-spectrum partial sums
+  int bins_out;         // tile_h * (tile_w/2 + 1), debug-output row length
+  size_t off_partial, off_coef, total;
+};
+ParPlan plan_par(int n_frames, int n_anchor, int Hg, int Wg, int D, const cast_par_params_t& p);
+
+cast_status_t launch_par(const float* resid, const int* anchors, int n_anchor, int n_frames,
+                         int Hg, int Wg, int D, const cast_par_params_t& p, float* out,
+                         float* theta_out, float* gate_out, float* conf_out,
+                         const ParPlan& plan, void* ws, hipStream_t stream);
+
+}  // namespace cast

@@ -1,0 +1,166 @@
+"""C ABI tests that need no GPU: the library loads, exports every symbol that
+include/cast.h declares, and each entry point rejects invalid arguments with the
+documented status before enqueueing anything (all checks here return before any
+HIP call).  Bypass rules of App. A.1 / App. B.3 return OK without work."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2609_34144_amd as cast
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cast.h")
+
+OK, NULL, SHAPE, ANCHORS, UNSUPPORTED, WORKSPACE = 0, 1, 2, 3, 4, 5
+
+# These tests pass fake (never dereferenced) device addresses: every call below has
+# at least one argument the validation rejects, so nothing is ever enqueued.  As a
+# second guard they only run where no GPU is visible.
+try:
+    import torch
+    _HAS_GPU = torch.cuda.is_available()
+except Exception:  # pragma: no cover
+    _HAS_GPU = False
+pytestmark = pytest.mark.skipif(_HAS_GPU, reason="fake-pointer validation tests run GPU-less only")
+A = 1 << 20   # a 256-byte aligned fake address
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(cast.LIB_PATH):
+        pytest.skip("libcast.so not built (run __graft_entry__.build())")
+    return cast.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cast_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("cast_route_kv", "cast_anchor_attn", "cast_par_reconstruct"):
+        assert required in names
+    assert set(names) == set(cast.EXPORTED)
+
+
+def test_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", cast.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r" T (cast_[a-z_]+)$", out, flags=re.M))
+    for name in declared_functions():
+        assert name in exported, name
+        assert hasattr(lib, name)
+
+
+def test_status_strings(lib):
+    for code, name in cast.STATUS_NAMES.items():
+        assert lib.cast_status_string(code).decode() == name
+    assert lib.cast_abi_version() == 1
+
+
+def test_par_params_default_matches_paper(lib):
+    """tab:config_cast: 8x8 tiles, (tau_low, tau_high, q, T) = (0.25, 0.75, 2, 0.10);
+    App. A.2: eta = 1e-6 max W + 1e-8, eps = 1e-8."""
+    p = cast.cast_par_params_default()
+    assert (p.tile_h, p.tile_w) == (8, 8)
+    assert abs(p.tau_low - 0.25) < 1e-7 and abs(p.tau_high - 0.75) < 1e-7
+    assert abs(p.q - 2.0) < 1e-7 and abs(p.T - 0.10) < 1e-7
+    assert abs(p.eta_rel - 1e-6) < 1e-12 and abs(p.eta_abs - 1e-8) < 1e-14
+    assert abs(p.eps - 1e-8) < 1e-14
+    assert p.gate_mode == 0 and p.accumulate == 0
+
+
+def _route(lib, *, q=A, k=2 * A, n_a=2, S=64, H=2, dh=32, M=4, Bv=64, topk=2, idx=3 * A, keff=True,
+           ws=None, wsb=0):
+    k_eff = ctypes.c_int(-7)
+    st = lib.cast_route_kv(q, k, n_a, S, H, dh, M, Bv, topk, 1.0, None, idx,
+                           ctypes.byref(k_eff) if keff else None, ws, wsb, None)
+    return st, k_eff.value
+
+
+def test_route_validation(lib):
+    assert _route(lib, keff=False)[0] == NULL
+    assert _route(lib, dh=96)[0] == UNSUPPORTED
+    assert _route(lib, M=5000)[0] == UNSUPPORTED
+    assert _route(lib, S=0)[0] == SHAPE
+    assert _route(lib, topk=0)[0] == SHAPE
+    assert _route(lib, q=None)[0] == NULL
+    assert _route(lib, idx=None)[0] == NULL
+    assert _route(lib, q=A + 8)[0] == SHAPE                       # misaligned
+    assert _route(lib, ws=None, wsb=0)[0] == WORKSPACE
+    need = lib.cast_route_kv_workspace_bytes(2, 64, 2, 32, 4, 64)
+    assert need > 0
+    assert _route(lib, ws=4 * A, wsb=need - 1)[0] == WORKSPACE  # too small
+    assert _route(lib, ws=4 * A + 8, wsb=need)[0] == WORKSPACE  # misaligned workspace
+
+
+def test_route_bypass_m0(lib):
+    """M == 0: routing is bypassed, k_eff = 0, nothing enqueued (App. B.3)."""
+    st, k_eff = _route(lib, q=None, k=None, idx=None, M=0)
+    assert st == OK and k_eff == 0
+    assert lib.cast_route_kv_workspace_bytes(2, 64, 2, 32, 0, 64) == 0
+
+
+def _attn(lib, *, q=A, k=2 * A, v=3 * A, idx=4 * A, k_eff=2, kc=None, vc=None, n0=0, n_a=2, S=64, H=2,
+          dh=32, M=4, Bv=64, scale=0.5, out=5 * A):
+    return lib.cast_anchor_attn(q, k, v, idx, k_eff, kc, vc, n0, n_a, S, H, dh, M, Bv, scale,
+                                out, None, None)
+
+
+def test_attn_validation(lib):
+    assert _attn(lib, dh=48) == UNSUPPORTED
+    assert _attn(lib, k_eff=5) == SHAPE                  # k_eff > M
+    assert _attn(lib, k_eff=0, n0=0) == SHAPE            # nothing to attend to
+    assert _attn(lib, scale=0.0) == SHAPE
+    assert _attn(lib, scale=float("nan")) == SHAPE
+    assert _attn(lib, q=None) == NULL
+    assert _attn(lib, idx=None) == NULL
+    assert _attn(lib, n0=4) == NULL                      # k_cur / v_cur missing
+    assert _attn(lib, out=5 * A + 8) == SHAPE                   # misaligned
+
+
+def _par(lib, anchors, *, n_frames=4, Hg=8, Wg=8, D=64, resid=A, out=2 * A, ws=None, wsb=0,
+         params=None, **pkw):
+    p = params if params is not None else cast.cast_par_params_default(**pkw)
+    arr = (ctypes.c_int * max(len(anchors), 1))(*anchors)
+    return lib.cast_par_reconstruct(resid, arr if anchors is not None else None, len(anchors),
+                                    n_frames, Hg, Wg, D, ctypes.byref(p), out, None, None, None,
+                                    ws, wsb, None)
+
+
+def test_par_validation(lib):
+    assert _par(lib, [0, 3], n_frames=4, resid=None) == NULL
+    assert _par(lib, [3, 0]) == ANCHORS                  # not increasing
+    assert _par(lib, [0, 0, 3]) == ANCHORS
+    assert _par(lib, [0, 4]) == ANCHORS                  # out of range
+    assert _par(lib, [1]) == ANCHORS                     # K_f < 2 (eq:block)
+    assert _par(lib, [0, 3], tile_h=9) == UNSUPPORTED
+    assert _par(lib, [0, 3], tile_w=0) == UNSUPPORTED
+    assert _par(lib, [0, 3], gate_mode=3) == SHAPE
+    assert _par(lib, [0, 3], T=0.0) == SHAPE
+    assert _par(lib, [0, 3], tau_low=0.8, tau_high=0.7) == SHAPE
+    assert _par(lib, [0, 3]) == WORKSPACE
+    assert lib.cast_par_reconstruct(A, None, 2, 4, 8, 8, 64,
+                                    ctypes.byref(cast.cast_par_params_default()), 2 * A, None,
+                                    None, None, None, 0, None) == NULL
+
+
+def test_par_bypass_all_anchors(lib):
+    """K_f = N_cur: every frame is computed, reconstruction is bypassed (App. A.1)."""
+    assert _par(lib, [0, 1, 2, 3], resid=None, out=None) == OK
+    assert _par(lib, [0], n_frames=1, resid=None, out=None) == OK
+    p = cast.cast_par_params_default()
+    assert lib.cast_par_workspace_bytes(4, 4, 8, 8, 64, ctypes.byref(p)) == 0
+
+
+def test_workspace_queries_grow_with_size(lib):
+    p = cast.cast_par_params_default()
+    small = lib.cast_par_workspace_bytes(4, 2, 8, 8, 64, ctypes.byref(p))
+    big = lib.cast_par_workspace_bytes(66, 2, 64, 64, 3072, ctypes.byref(p))
+    assert 0 < small < big
+    assert big % 256 == 0

@@ -1,0 +1,321 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle on
+identical seeded inputs.
+
+Bars (written here, used everywhere below):
+  routing indices   bit-exact wherever the oracle's fp32 K-th / (K+1)-th score gap
+                    exceeds the fp32 accumulation bound; inside that bound the
+                    selection must be a valid TopK of the oracle scores
+  attention         max-abs <= 2e-2 and rel-RMS <= 5e-3 over the whole output
+  PAR               rel-RMS <= 1e-4 over the written skipped-frame slots; anchor
+                    slots of `out` bit-identical to what they held before
+rel-RMS = ||x - y||_2 / ||y||_2.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import gen
+from gen import workloads as W
+from oracle import attn as OA
+from oracle import par as OP
+from oracle import route as OR
+
+pytestmark = pytest.mark.gpu
+
+ATTN_MAX_ABS, ATTN_REL_RMS = 2e-2, 5e-3
+PAR_REL_RMS = 1e-4
+
+
+def rel_rms(x, y):
+    x = np.asarray(x, np.float64)
+    y = np.asarray(y, np.float64)
+    return float(np.linalg.norm((x - y).ravel()) / max(np.linalg.norm(y.ravel()), 1e-300))
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+def np64(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+# ---------------------------------------------------------------------------
+# routing
+# ---------------------------------------------------------------------------
+
+def check_route(cast_lib, q, k, topk, scale, label):
+    idx, k_eff, scores = cast_lib.cast_route_kv(q, k, topk, scale, want_scores=True)
+    torch.cuda.synchronize()
+    s_or = OR.chunk_scores(np64(q), np64(k), scale)                 # fp64
+    n_a, H, M = s_or.shape
+    assert k_eff == min(topk, M)
+    s_gpu = scores.cpu().numpy().astype(np.float64)
+    smax = np.abs(s_or).max() + 1e-30
+    tol = 1e-4 * smax + 1e-7
+    assert np.abs(s_gpu - s_or).max() <= tol, (label, np.abs(s_gpu - s_or).max(), tol)
+    s32 = s_or.astype(np.float32)
+    g = idx.cpu().numpy()
+    exact = near = 0
+    for i in range(n_a):
+        for h in range(H):
+            want = OR.topk_select(s32[i, h], k_eff)
+            got = [int(x) for x in g[i, h]]
+            assert got == sorted(got), "indices must be ascending"
+            assert len(set(got)) == k_eff and all(0 <= x < M for x in got)
+            order = sorted(range(M), key=lambda m: (-float(s32[i, h, m]), m))
+            kth = float(s32[i, h, order[k_eff - 1]])
+            nxt = float(s32[i, h, order[k_eff]]) if k_eff < M else -math.inf
+            if kth - nxt > 2 * tol:
+                assert got == want, (label, i, h, got, want)
+                exact += 1
+            else:
+                near += 1
+                sel = set(got)
+                for m in range(M):
+                    if m in sel:
+                        assert s_or[i, h, m] >= kth - 2 * tol
+                    else:
+                        assert s_or[i, h, m] <= kth + 2 * tol
+    log(f"[route {label}] exact rows {exact}, near-tie rows {near}, max|ds| "
+        f"{np.abs(s_gpu - s_or).max():.2e}")
+    return idx, k_eff
+
+
+def test_route_tiny(cast_lib):
+    w = gen.get(W.TINY)
+    q, k, v, _, _ = gen.attn_inputs(w, seed=42, device="cuda")
+    check_route(cast_lib, q, k, w.topk, 1.0, "tiny")
+
+
+def test_route_matrix_like(cast_lib):
+    w = gen.get(W.MATRIX)
+    q, k, v, _, _ = gen.attn_inputs(w, seed=42, device="cuda")
+    check_route(cast_lib, q, k, w.topk, w.scale, "matrix")
+
+
+def test_route_ties_and_budget(cast_lib):
+    """Byte-identical chunks score identically on both sides: the lower index wins
+    (exact tie rule); topk >= M keeps every chunk (App. B.3)."""
+    w = gen.get(W.TINY)
+    q, k, _, _, _ = gen.attn_inputs(w, seed=7, device="cuda", M=9, Bv=40,
+                                    duplicate_chunks=[(5, 2), (8, 2), (7, 0)])
+    idx, k_eff, scores = cast_lib.cast_route_kv(q, k, 1, 1.0, want_scores=True)
+    torch.cuda.synchronize()
+    s = scores.cpu().numpy()
+    assert np.array_equal(s[:, :, 5], s[:, :, 2]) and np.array_equal(s[:, :, 8], s[:, :, 2])
+    g = idx.cpu().numpy()
+    for i in range(g.shape[0]):
+        for h in range(g.shape[1]):
+            best = max(range(9), key=lambda m: (float(s[i, h, m]), -m))
+            assert int(g[i, h, 0]) == best
+            assert best not in (5, 8, 7)           # a duplicate never beats its lower twin
+    idx_all, k_all, _ = cast_lib.cast_route_kv(q, k, 50, 1.0)
+    torch.cuda.synchronize()
+    assert k_all == 9
+    assert np.array_equal(idx_all.cpu().numpy(), np.tile(np.arange(9), (2, 2, 1)))
+    check_route(cast_lib, q, k, 4, 0.3, "ties")
+
+
+def test_route_deterministic(cast_lib):
+    w = gen.get(W.MATRIX)
+    q, k, _, _, _ = gen.attn_inputs(w, seed=3, device="cuda")
+    a = cast_lib.cast_route_kv(q, k, 4, 0.1, want_scores=True)
+    b = cast_lib.cast_route_kv(q, k, 4, 0.1, want_scores=True)
+    torch.cuda.synchronize()
+    assert torch.equal(a[0], b[0]) and torch.equal(a[2], b[2])
+
+
+# ---------------------------------------------------------------------------
+# attention
+# ---------------------------------------------------------------------------
+
+def check_attn(cast_lib, q, k, v, idx, k_eff, scale, kc=None, vc=None, rows=None, label=""):
+    out, lse = cast_lib.cast_anchor_attn(q, k, v, idx, k_eff, scale, k_cur=kc, v_cur=vc,
+                                         want_lse=True)
+    torch.cuda.synchronize()
+    O, L = OA.anchor_attention(np64(q), np64(k), np64(v), idx.cpu().numpy() if idx is not None
+                               else np.zeros((q.shape[0], q.shape[2], 0), np.int32), scale,
+                               k_cur=None if kc is None else np64(kc),
+                               v_cur=None if vc is None else np64(vc), rows=rows)
+    got = np64(out)
+    lg = lse.cpu().numpy().astype(np.float64)
+    if rows is not None:
+        sel = tuple(np.array(r) for r in zip(*[(i, s, h) for (i, h, s) in rows]))
+        got, O = got[sel], O[sel]
+        lsel = tuple(np.array(r) for r in zip(*[(i, h, s) for (i, h, s) in rows]))
+        lg, L = lg[lsel], L[lsel]
+    mx = np.abs(got - O).max()
+    rr = rel_rms(got, O)
+    log(f"[attn {label}] max-abs {mx:.3e} rel-RMS {rr:.3e} lse max-abs {np.abs(lg - L).max():.2e}")
+    assert mx <= ATTN_MAX_ABS and rr <= ATTN_REL_RMS, (label, mx, rr)
+    assert np.abs(lg - L).max() <= 1e-3 * max(1.0, np.abs(L).max())
+    return out
+
+
+def test_attn_tiny(cast_lib):
+    w = gen.get(W.TINY)
+    q, k, v, _, _ = gen.attn_inputs(w, seed=42, device="cuda")
+    idx, k_eff = check_route(cast_lib, q, k, w.topk, 1.0, "tiny")
+    check_attn(cast_lib, q, k, v, idx, k_eff, w.scale, label="tiny")
+
+
+@pytest.mark.parametrize("dh", [32, 64, 128])
+def test_attn_shapes_and_ragged_tails(cast_lib, dh):
+    """Several 128-query tiles plus a ragged query tail; a key sequence that is
+    not a multiple of the 64-key tile; chunk lengths that straddle tiles; an
+    always-attended current segment; routed indices in arbitrary order."""
+    torch.manual_seed(dh)
+    n_a, S, H, M, Bv, n0 = 2, 300, 3, 7, 45, 19
+    dev = "cuda"
+    q = torch.randn(n_a, S, H, dh, device=dev).to(torch.bfloat16)
+    k = torch.randn(M, Bv, H, dh, device=dev).to(torch.bfloat16)
+    v = torch.randn(M, Bv, H, dh, device=dev).to(torch.bfloat16)
+    kc = torch.randn(n0, H, dh, device=dev).to(torch.bfloat16)
+    vc = torch.randn(n0, H, dh, device=dev).to(torch.bfloat16)
+    idx = torch.tensor([[[6, 1, 3], [0, 2, 5], [4, 4, 1]], [[2, 3, 6], [5, 0, 1], [6, 5, 4]]],
+                       dtype=torch.int32, device=dev)
+    check_attn(cast_lib, q, k, v, idx, 3, 1 / math.sqrt(dh), kc=kc, vc=vc, label=f"ragged dh{dh}")
+    # current segment only (k_eff = 0) and history only (n0 = 0)
+    check_attn(cast_lib, q, k, v, idx[:, :, :0].contiguous(), 0, 1 / math.sqrt(dh), kc=kc, vc=vc,
+               label=f"n0-only dh{dh}")
+    check_attn(cast_lib, q, k, v, idx, 3, 1 / math.sqrt(dh), label=f"hist-only dh{dh}")
+
+
+def test_attn_topk_all_equals_dense(cast_lib):
+    """topk = M routes every chunk: the result is dense attention over the whole history."""
+    w = gen.get(W.TINY)
+    q, k, v, _, _ = gen.attn_inputs(w, seed=5, device="cuda")
+    idx, k_eff, _ = cast_lib.cast_route_kv(q, k, w.M, 1.0)
+    assert k_eff == w.M
+    out = check_attn(cast_lib, q, k, v, idx, k_eff, w.scale, label="dense")
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        q.float().permute(0, 2, 1, 3),
+        k.float().permute(2, 0, 1, 3).reshape(1, w.H, w.M * w.Bv, w.dh).expand(w.n_a, -1, -1, -1),
+        v.float().permute(2, 0, 1, 3).reshape(1, w.H, w.M * w.Bv, w.dh).expand(w.n_a, -1, -1, -1),
+        scale=w.scale).permute(0, 2, 1, 3)
+    assert (out.float() - ref).abs().max().item() <= ATTN_MAX_ABS
+
+
+def test_attn_matrix_like_sampled(cast_lib):
+    """Full Matrix-Game-like shapes (3 anchors x 12 heads x 1560 queries over 4 routed
+    chunks of 1560 tokens), checked on sampled query rows of every (anchor, head)."""
+    w = gen.get(W.MATRIX)
+    q, k, v, _, _ = gen.attn_inputs(w, seed=42, device="cuda")
+    idx, k_eff = check_route(cast_lib, q, k, w.topk, w.scale, "matrix")
+    rng = np.random.default_rng(0)
+    rows = [(i, h, int(s)) for i in range(w.n_a) for h in range(w.H)
+            for s in list(rng.choice(w.S, 24, replace=False)) + [0, w.S - 1, 1535, 1536]]
+    check_attn(cast_lib, q, k, v, idx, k_eff, w.scale, rows=rows, label="matrix sampled")
+
+
+def test_attn_deterministic(cast_lib):
+    w = gen.get(W.TINY)
+    q, k, v, _, _ = gen.attn_inputs(w, seed=11, device="cuda")
+    idx, k_eff, _ = cast_lib.cast_route_kv(q, k, 2, 1.0)
+    a, _ = cast_lib.cast_anchor_attn(q, k, v, idx, k_eff, w.scale)
+    b, _ = cast_lib.cast_anchor_attn(q, k, v, idx, k_eff, w.scale)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+# ---------------------------------------------------------------------------
+# PAR
+# ---------------------------------------------------------------------------
+
+def run_par(cast_lib, resid_np, anchors, *, accumulate=False, gate_mode=0, x0=None, tile=8,
+            debug=False):
+    dev = "cuda"
+    resid = torch.from_numpy(resid_np.astype(np.float32)).to(dev)
+    prm = cast_lib.cast_par_params_default(accumulate=int(accumulate), gate_mode=gate_mode,
+                                           tile_h=tile, tile_w=tile)
+    if x0 is None:
+        out = torch.full_like(resid, -7.25)            # sentinel: anchor slots must keep it
+    else:
+        out = torch.from_numpy(x0.astype(np.float32)).to(dev)
+    before = out.clone()
+    th = gt = cf = None
+    if debug:
+        s1, s2 = cast_lib.par_debug_shapes(len(anchors), resid.shape[1], resid.shape[2], prm)
+        th = torch.full(s1, 99.0, device=dev)
+        gt = torch.full(s1, 99.0, device=dev)
+        cf = torch.full(s2, 99.0, device=dev)
+    cast_lib.cast_par_reconstruct(resid, anchors, prm, out=out, theta_out=th, gate_out=gt,
+                                  conf_out=cf)
+    torch.cuda.synchronize()
+    return out, before, prm, (th, gt, cf)
+
+
+def check_par(cast_lib, resid_np, anchors, *, accumulate=False, gate_mode=0, x0=None, tile=8,
+              targets=None, label="", debug=False):
+    n = resid_np.shape[0]
+    out, before, prm, dbg = run_par(cast_lib, resid_np, anchors, accumulate=accumulate,
+                                    gate_mode=gate_mode, x0=x0, tile=tile, debug=debug)
+    oprm = OP.ParParams(tile_h=tile, tile_w=tile, gate_mode=gate_mode, accumulate=accumulate)
+    ref = OP.par_reconstruct(resid_np.astype(np.float64), anchors, oprm,
+                             out=None if x0 is None else x0.astype(np.float64), targets=targets)
+    got = out.cpu().numpy().astype(np.float64)
+    skipped = [t for t in range(n) if t not in set(anchors)]
+    check_t = skipped if targets is None else [t for t in skipped if t in targets]
+    rr = rel_rms(got[check_t], ref[check_t])
+    log(f"[par {label}] rel-RMS {rr:.3e} over {len(check_t)} frames")
+    assert rr <= PAR_REL_RMS, (label, rr)
+    for a in anchors:
+        assert torch.equal(out[a], before[a]), f"anchor slot {a} was written"
+    if debug:
+        th, gt, cf = (t.cpu().numpy().astype(np.float64) for t in dbg)
+        th_o, g_o, c_o = OP.stats_arrays(resid_np.astype(np.float64), anchors, oprm)
+        assert np.abs(cf - c_o).max() <= 1e-4, np.abs(cf - c_o).max()
+        assert np.abs(gt - g_o).max() <= 1e-3, np.abs(gt - g_o).max()
+        dth = np.abs(th - th_o)
+        dth = np.minimum(dth, 2 * np.pi - dth)
+        assert dth.max() <= 1e-3, dth.max()
+    return out
+
+
+def test_par_tiny_all_modes(cast_lib):
+    w = gen.get(W.TINY)
+    resid, x0, _ = gen.par_inputs(w, seed=42)
+    for gm in (0, 1, 2):
+        check_par(cast_lib, resid, w.anchors, gate_mode=gm, label=f"tiny gate{gm}", debug=True)
+    check_par(cast_lib, resid, w.anchors, accumulate=True, x0=x0, label="tiny acc")
+
+
+def test_par_edge_tiles_and_ragged_channels(cast_lib):
+    """Grids whose edges leave 6-, 5-, 3- and 1-wide tiles, channel counts that are not a
+    multiple of the 64-lane block, boundary extrapolation on both sides, K_f = 2."""
+    rng = np.random.default_rng(1)
+    for (n, Hg, Wg, D, anchors) in [(7, 14, 13, 80, (2, 5)), (6, 17, 9, 33, (0, 2, 5)),
+                                    (5, 30, 52, 64, (1, 3))]:
+        base = rng.standard_normal((Hg, Wg, D))
+        resid = np.zeros((n, Hg, Wg, D))
+        for j, a in enumerate(anchors):
+            resid[a] = np.roll(base, (j, 2 * j), axis=(0, 1)) + 0.3 * rng.standard_normal((Hg, Wg, D))
+        check_par(cast_lib, resid, anchors, label=f"edges {Hg}x{Wg}x{D}", debug=True)
+        x0 = rng.standard_normal(resid.shape)
+        check_par(cast_lib, resid, anchors, accumulate=True, x0=x0, label=f"edges acc {Hg}x{Wg}")
+
+
+def test_par_small_tiles(cast_lib):
+    """Tile parameter other than 8 (4x4 tiles, remainder 3)."""
+    rng = np.random.default_rng(2)
+    base = rng.standard_normal((11, 11, 16))
+    resid = np.stack([base, np.roll(base, (1, 0), axis=(0, 1)), np.zeros_like(base),
+                      np.roll(base, (2, 1), axis=(0, 1))])
+    check_par(cast_lib, resid, (0, 1, 3), tile=4, label="tile4", debug=True)
+
+
+def test_par_matrix_like(cast_lib):
+    w = gen.get(W.MATRIX)
+    resid, _, _ = gen.par_inputs(w, seed=42)
+    check_par(cast_lib, resid, w.anchors, label="matrix write", debug=True)
+
+
+def test_par_deterministic(cast_lib):
+    w = gen.get(W.MATRIX)
+    resid, _, _ = gen.par_inputs(w, seed=1)
+    a, _, _, _ = run_par(cast_lib, resid, w.anchors)
+    b, _, _, _ = run_par(cast_lib, resid, w.anchors)
+    assert torch.equal(a, b)
