@@ -1,0 +1,232 @@
+"""Benchmark of one CAST block step on one MI355X.
+
+A step is the whole hot path on one batch of synthetic input, stream-ordered on
+torch's current stream:  cast_route_kv -> cast_anchor_attn -> cast_par_reconstruct
+(accumulate mode, X_t += R_hat_t).  Inputs are resident in HBM before timing;
+the step cycles over several copies of its inputs so that consecutive steps do
+not find their inputs in the Infinity Cache.
+
+Prints ONE JSON line.  `value` = frame-tokens/s = N_cur * S / step time.
+`roofline` describes the dominant kernel (routed attention: bf16 MFMA); the
+per-call figures for routing and PAR are reported beside it.  `cpu_baseline`
+times the float64 oracle on a bounded sample of the same workload on this host.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+N_COPIES = 4                   # input copies cycled through (> Infinity Cache)
+
+
+def attn_flops(w, k_eff):
+    """Useful FLOPs of routed attention: 4 S (n0 + K Bv) dh per (anchor, head)."""
+    return 4.0 * w.S * (w.n0 + k_eff * w.Bv) * w.dh * w.H * w.n_a
+
+
+def route_bytes(w):
+    """Algorithmic bytes of routing: one read of K history and of the anchor Q (bf16)."""
+    return 2.0 * (w.M * w.Bv + w.n_a * w.S) * w.H * w.dh
+
+
+def par_bytes(w, accumulate=True):
+    """Algorithmic bytes of PAR: anchors read once; skipped frames written, and read
+    too when accumulating (fp32)."""
+    frame = 4.0 * w.S * w.D
+    n_skip = w.n_frames - w.n_a
+    return frame * (w.n_a + n_skip * (2 if accumulate else 1))
+
+
+def cpu_baseline(w, seed=42, attn_pairs=2):
+    """The oracle as it stands, timed on this host on a bounded sample of the
+    workload: full routing, `attn_pairs` of the n_a*H (anchor, head) attention
+    pairs (scaled by the pair count), and PAR on every skipped frame."""
+    import numpy as np
+    import torch
+    import gen
+    from oracle import attn as OA
+    from oracle import par as OP
+    from oracle import route as OR
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        threads = 1
+    cores = len(os.sched_getaffinity(0))
+    q, k, v, _, _ = gen.attn_inputs(w, seed=seed, device="cpu")
+    qn, kn, vn = (t.float().numpy().astype(np.float64) for t in (q, k, v))
+    resid, x0, _ = gen.par_inputs(w, seed=seed)
+    t0 = time.perf_counter()
+    _, idx, k_eff = OR.route(qn, kn, w.topk, w.scale, decide_dtype=np.float32)
+    t_route = time.perf_counter() - t0
+    pairs = [(i, h) for i in range(w.n_a) for h in range(w.H)][:attn_pairs]
+    rows = [(i, h, s) for (i, h) in pairs for s in range(w.S)]
+    t0 = time.perf_counter()
+    OA.anchor_attention(qn, kn, vn, idx, w.scale, rows=rows)
+    t_attn = (time.perf_counter() - t0) * (w.n_a * w.H) / len(pairs)
+    t0 = time.perf_counter()
+    OP.par_reconstruct(resid.astype(np.float64), w.anchors, OP.ParParams(accumulate=True),
+                       out=x0.astype(np.float64) if x0 is not None else None)
+    t_par = time.perf_counter() - t0
+    total = t_route + t_attn + t_par
+    return {
+        "value": w.frame_tokens / total, "unit": "frame-tokens/s", "cores": max(threads, 1),
+        "host_cores_visible": cores, "kind": "oracle",
+        "sample": (f"{w.name}: full routing ({t_route:.2f} s), attention on {len(pairs)} of "
+                   f"{w.n_a * w.H} (anchor, head) pairs scaled x{w.n_a * w.H / len(pairs):.0f} "
+                   f"({t_attn:.2f} s extrapolated), full PAR accumulate ({t_par:.2f} s); "
+                   f"float64 numpy, BLAS threads {threads}"),
+        "seconds": {"route": t_route, "attn_extrapolated": t_attn, "par": t_par},
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="matrix_game_like_8f30x52_d1536")
+    ap.add_argument("--seed", type=int, default=42)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one MI355X only (got --gpus {args.gpus}); the hot path is "
+              f"built and measured on one GPU, multi-GPU sharding is not part of it.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import gen
+    import paper_2609_34144_amd as cast
+
+    w = gen.get(args.workload)
+    cast.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+
+    # ---- inputs (resident in HBM), N_COPIES copies at distinct addresses
+    q, k, v, kc, vc = gen.attn_inputs(w, seed=args.seed, device=dev) if w.has_attention else \
+        (None,) * 5
+    resid_np, _, _ = gen.par_inputs(w, seed=args.seed)
+    resid = torch.from_numpy(resid_np).to(dev)
+    del resid_np
+    sets = []
+    for c in range(N_COPIES):
+        s = {"resid": resid.clone(), "x": torch.randn(resid.shape, device=dev, dtype=torch.float32)}
+        if w.has_attention:
+            s.update(q=q.clone(), k=k.clone(), v=v.clone())
+        sets.append(s)
+    del q, k, v, resid
+    prm = cast.cast_par_params_default(accumulate=1)
+    k_eff = min(w.topk, w.M) if w.has_attention else 0
+    route_ws = par_ws = None
+    if w.has_attention and w.M > 0:
+        nb = cast.cast_route_kv_workspace_bytes(w.n_a, w.S, w.H, w.dh, w.M, w.Bv)
+        route_ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+    if w.has_par:
+        nb = cast.cast_par_workspace_bytes(w.n_frames, w.n_a, w.Hg, w.Wg, w.D, prm)
+        par_ws = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
+    idx = torch.empty((w.n_a, w.H, max(k_eff, 1)), dtype=torch.int32, device=dev)
+    attn_out = torch.empty((w.n_a, w.S, w.H, w.dh), dtype=torch.bfloat16, device=dev) \
+        if w.has_attention else None
+
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def step(s, marks=None):
+        if marks is not None:
+            marks[0].record(stream)
+        if w.has_attention:
+            _, ke, _ = cast.cast_route_kv(s["q"], s["k"], w.topk, w.scale, idx_out=idx,
+                                          workspace=route_ws, stream=stream)
+            if marks is not None:
+                marks[1].record(stream)
+            cast.cast_anchor_attn(s["q"], s["k"], s["v"], idx, ke, w.scale, out=attn_out,
+                                  stream=stream)
+        elif marks is not None:
+            marks[1].record(stream)
+        if marks is not None:
+            marks[2].record(stream)
+        if w.has_par:
+            cast.cast_par_reconstruct(s["resid"], w.anchors, prm, out=s["x"], workspace=par_ws,
+                                      stream=stream)
+        if marks is not None:
+            marks[3].record(stream)
+
+    for i in range(args.warmup):
+        step(sets[i % N_COPIES])
+    torch.cuda.synchronize()
+
+    marks = [[ev() for _ in range(4)] for _ in range(args.steps)]
+    t_start, t_end = ev(), ev()
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(args.steps):
+        step(sets[i % N_COPIES], marks[i])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms_total = t_start.elapsed_time(t_end)
+    ms_step = ms_total / args.steps
+    route_ms = float(np.mean([m[0].elapsed_time(m[1]) for m in marks]))
+    attn_ms = float(np.mean([m[1].elapsed_time(m[2]) for m in marks]))
+    par_ms = float(np.mean([m[2].elapsed_time(m[3]) for m in marks]))
+
+    value = w.frame_tokens / (ms_step / 1e3)
+    res = {
+        "metric": "CAST block-step frame-tokens/s (routing + routed anchor attention + PAR)",
+        "value": value, "unit": "frame-tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16+fp32",
+        "data": "synthetic (seeded; shapes of the paper's Matrix-Game-like block)",
+        "config": {"workload": w.name, "frames": w.n_frames, "grid": f"{w.Hg}x{w.Wg}",
+                   "D": w.D, "heads": w.H, "dh": w.dh, "anchors": list(w.anchors),
+                   "history_chunks": w.M, "chunk_tokens": w.Bv, "topk": w.topk,
+                   "par_mode": "accumulate", "input_copies": N_COPIES},
+        "per_call_ms": {"route": route_ms, "attn": attn_ms, "par": par_ms},
+    }
+    extra = {}
+    if w.has_attention:
+        fl = attn_flops(w, k_eff)
+        tf = fl / (attn_ms / 1e3) / 1e12
+        res["roofline"] = {"bound": "mfma", "kernel": "anchor_attn_kernel<128>",
+                           "achieved": tf, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                           "frac": tf / PEAK_BF16_TFLOPS, "traffic": None,
+                           "algorithmic_per_launch": fl}
+        extra["attn_mfma_util_pct"] = 100.0 * tf / PEAK_BF16_TFLOPS
+        rg = route_bytes(w) / (route_ms / 1e3) / 1e9
+        extra["route_hbm_gbps"] = rg
+        extra["route_hbm_pct"] = 100.0 * rg / PEAK_HBM_GBS
+    if w.has_par:
+        pg = par_bytes(w, True) / (par_ms / 1e3) / 1e9
+        extra["par_hbm_gbps"] = pg
+        extra["par_hbm_pct"] = 100.0 * pg / PEAK_HBM_GBS
+        if not w.has_attention:
+            res["roofline"] = {"bound": "hbm", "kernel": "par (xspec+gate+recon)",
+                               "achieved": pg, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                               "frac": pg / PEAK_HBM_GBS, "traffic": None,
+                               "algorithmic_per_launch": par_bytes(w, True)}
+    res.update(extra)
+    if not args.no_cpu_baseline:
+        try:
+            res["cpu_baseline"] = cpu_baseline(w, seed=args.seed)
+        except Exception as e:  # reported, never fatal for the GPU measurement
+            res["cpu_baseline"] = {"value": None, "error": repr(e)}
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

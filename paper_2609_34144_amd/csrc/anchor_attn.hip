@@ -28,10 +28,13 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kBQ = 128;   // queries per workgroup
 constexpr int kBK = 64;    // keys per tile
 constexpr int kThreads = 256;
+constexpr int kMaxKeff = kAttnMaxKeff;   // routed chunk indices cached in LDS
 
 struct AttnArgs {
   const uint16_t* q;
@@ -54,17 +57,20 @@ __device__ __forceinline__ int xcd_remap(int b, int nb) {
   return (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + j;
 }
 
+// Address of key/value row r of the (anchor, head) sequence [current ; routed chunks].
+// Rows past the end are clamped to the last row (their logits are masked, so they
+// contribute exactly zero); chunk indices come from the LDS copy `sidx`.
 template <int DH>
 __device__ __forceinline__ const uint16_t* row_ptr(const AttnArgs& a, const uint16_t* hist,
-                                                   const uint16_t* cur, const int32_t* idx_ih,
-                                                   int r, int h) {
-  if (r < a.n0) return cur + ((long long)r * a.H + h) * DH;
-  const unsigned rr = (unsigned)(r - a.n0);
+                                                   const uint16_t* cur, const int* sidx, int r,
+                                                   int h) {
+  r = r < a.L ? r : a.L - 1;
+  const unsigned rr = (unsigned)max(r - a.n0, 0);
   const unsigned slot = (unsigned)(((unsigned long long)rr * a.bv_magic) >> 40);
   const unsigned t = rr - slot * (unsigned)a.Bv;
-  int c = idx_ih[slot];
-  c = c < 0 ? 0 : (c >= a.M ? a.M - 1 : c);
-  return hist + (((long long)c * a.Bv + t) * a.H + h) * DH;
+  const uint16_t* hp = hist + (((long long)sidx[slot] * a.Bv + t) * a.H + h) * DH;
+  const uint16_t* cp = cur + ((long long)r * a.H + h) * DH;
+  return r < a.n0 ? cp : hp;
 }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -92,80 +98,78 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
   using T = Tile<DH>;
   __shared__ __attribute__((aligned(16))) uint16_t lds_k[2][T::K_ELEMS];
   __shared__ __attribute__((aligned(16))) uint16_t lds_v[2][T::V_ELEMS];
+  __shared__ int sidx[kMaxKeff];
 
   const int logical = xcd_remap(blockIdx.x, a.nblocks);
   const int pair = logical / a.n_qt, qt = logical - pair * a.n_qt;
   const int i = pair / a.H, h = pair - (pair / a.H) * a.H;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int l32 = lane & 31, hf = lane >> 5;
-  const int32_t* idx_ih = a.idx ? a.idx + ((long long)i * a.H + h) * a.k_eff : nullptr;
+  // routed chunk indices of this (anchor, head), clamped into [0, M)
+  if (a.k_eff > 0) {
+    const int32_t* idx_ih = a.idx + ((long long)i * a.H + h) * a.k_eff;
+    for (int j = tid; j < a.k_eff; j += kThreads) {
+      const int c = idx_ih[j];
+      sidx[j] = c < 0 ? 0 : (c >= a.M ? a.M - 1 : c);
+    }
+  } else if (tid == 0) {
+    sidx[0] = 0;
+  }
 
   // ---- Q^T operand in registers: lane holds query l32, d = 16t + 8hf .. +8
   const int qi = qt * kBQ + wave * 32 + l32;
   bf16x8 qreg[DH / 16];
   {
-    const bool ok = qi < a.S;
-    const uint16_t* qp = a.q + (((long long)i * a.S + (ok ? qi : 0)) * a.H + h) * DH + 8 * hf;
+    // rows past S load the last query; their outputs are never stored
+    const int qc = qi < a.S ? qi : a.S - 1;
+    const uint16_t* qp = a.q + (((long long)i * a.S + qc) * a.H + h) * DH + 8 * hf;
 #pragma unroll
-    for (int t = 0; t < DH / 16; ++t) {
-      uint4 v = ok ? *reinterpret_cast<const uint4*>(qp + 16 * t) : make_uint4(0, 0, 0, 0);
-      qreg[t] = __builtin_bit_cast(bf16x8, v);
-    }
+    for (int t = 0; t < DH / 16; ++t)
+      qreg[t] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qp + 16 * t));
   }
+  __syncthreads();   // sidx visible to every wave
 
   // ---- tile loaders (global -> registers -> LDS)
-  uint4 kbuf[T::KPASS];
-  uint4 vbuf[T::VPASS][4];
-  auto load_tile = [&](int tile) {
+  u32x4 kbuf[T::KPASS];
+  u32x4 vbuf[T::VPASS][4];
+  auto load_tile = [&](int tile) __attribute__((always_inline)) {
     const int r0 = tile * kBK;
 #pragma unroll
-    for (int p = 0; p < T::KPASS; ++p) {
-      const int r = r0 + p * T::RPP + tid / T::CPR;
-      kbuf[p] = make_uint4(0, 0, 0, 0);
-      if (r < a.L) {
-        const uint16_t* src = row_ptr<DH>(a, a.k, a.kc, idx_ih, r, h);
-        kbuf[p] = *reinterpret_cast<const uint4*>(src + (tid % T::CPR) * 8);
-      }
-    }
+    for (int p = 0; p < T::KPASS; ++p)
+      kbuf[p] = *reinterpret_cast<const u32x4*>(
+          row_ptr<DH>(a, a.k, a.kc, sidx, r0 + p * T::RPP + tid / T::CPR, h) + (tid % T::CPR) * 8);
 #pragma unroll
     for (int p = 0; p < T::VPASS; ++p) {
-      const int it = tid + p * kThreads;
+      const int it = min(tid + p * kThreads, T::VITEMS - 1);
       const int g = it / T::CPR, ch = it % T::CPR;
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const int r = r0 + 4 * g + kk;
-        vbuf[p][kk] = make_uint4(0, 0, 0, 0);
-        if (it < T::VITEMS && r < a.L) {
-          const uint16_t* src = row_ptr<DH>(a, a.v, a.vc, idx_ih, r, h);
-          vbuf[p][kk] = *reinterpret_cast<const uint4*>(src + ch * 8);
-        }
-      }
+      for (int kk = 0; kk < 4; ++kk)
+        vbuf[p][kk] = *reinterpret_cast<const u32x4*>(
+            row_ptr<DH>(a, a.v, a.vc, sidx, r0 + 4 * g + kk, h) + ch * 8);
     }
   };
-  auto store_tile = [&](int buf) {
+  auto store_tile = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int p = 0; p < T::KPASS; ++p) {
       const int row = p * T::RPP + tid / T::CPR;
-      *reinterpret_cast<uint4*>(&lds_k[buf][row * T::KSTR + (tid % T::CPR) * 8]) = kbuf[p];
+      *reinterpret_cast<u32x4*>(&lds_k[buf][row * T::KSTR + (tid % T::CPR) * 8]) = kbuf[p];
     }
 #pragma unroll
     for (int p = 0; p < T::VPASS; ++p) {
       const int it = tid + p * kThreads;
       if (it < T::VITEMS) {
         const int g = it / T::CPR, ch = it % T::CPR;
-        const uint32_t* v0 = reinterpret_cast<const uint32_t*>(&vbuf[p][0]);
-        const uint32_t* v1 = reinterpret_cast<const uint32_t*>(&vbuf[p][1]);
-        const uint32_t* v2 = reinterpret_cast<const uint32_t*>(&vbuf[p][2]);
-        const uint32_t* v3 = reinterpret_cast<const uint32_t*>(&vbuf[p][3]);
-        uint4* dst = reinterpret_cast<uint4*>(&lds_v[buf][(g * DH + ch * 8) * 4]);
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          // d = 8ch + 2w (low halves) and d = 8ch + 2w + 1 (high halves), keys 4g..4g+3
-          dst[w] = make_uint4(__builtin_amdgcn_perm(v1[w], v0[w], 0x05040100u),
-                              __builtin_amdgcn_perm(v3[w], v2[w], 0x05040100u),
-                              __builtin_amdgcn_perm(v1[w], v0[w], 0x07060302u),
-                              __builtin_amdgcn_perm(v3[w], v2[w], 0x07060302u));
-        }
+        const u32x4 v0 = vbuf[p][0], v1 = vbuf[p][1], v2 = vbuf[p][2], v3 = vbuf[p][3];
+        u32x4* dst = reinterpret_cast<u32x4*>(&lds_v[buf][(g * DH + ch * 8) * 4]);
+        // word w of a row holds d = 8ch + 2w (low half) and 8ch + 2w + 1 (high half);
+        // the LDS copy wants, per d, the 4 keys 4g..4g+3 side by side
+#define CAST_VT(w)                                                                   \
+  dst[w] = u32x4{__builtin_amdgcn_perm(v1[w], v0[w], 0x05040100u),                   \
+                 __builtin_amdgcn_perm(v3[w], v2[w], 0x05040100u),                   \
+                 __builtin_amdgcn_perm(v1[w], v0[w], 0x07060302u),                   \
+                 __builtin_amdgcn_perm(v3[w], v2[w], 0x07060302u)};
+        CAST_VT(0) CAST_VT(1) CAST_VT(2) CAST_VT(3)
+#undef CAST_VT
       }
     }
   };
@@ -195,7 +199,7 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
       const uint16_t* kr = &lds_k[buf][(kb * 32 + l32) * T::KSTR + 8 * hf];
 #pragma unroll
       for (int t = 0; t < DH / 16; ++t) {
-        bf16x8 ka = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kr + 16 * t));
+        bf16x8 ka = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kr + 16 * t));
         acc_s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[t], acc_s[kb], 0, 0, 0);
       }
     }
@@ -218,7 +222,7 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
       for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc_s[kb][e]);
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float m_new = fmaxf(m_run, mx * a.sl2);
-    const float corr = exp2f(m_run - m_new);
+    const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
     float rs = 0.0f;
     bf16x8 pb[2][2];
 #pragma unroll
@@ -226,13 +230,13 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
       float p[16];
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        p[e] = exp2f(fmaf(acc_s[kb][e], a.sl2, -m_new));
+        p[e] = __builtin_amdgcn_exp2f(fmaf(acc_s[kb][e], a.sl2, -m_new));
         rs += p[e];
       }
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
-        uint4 w = make_uint4(pack_bf16x2(p[8 * s + 0], p[8 * s + 1]), pack_bf16x2(p[8 * s + 2], p[8 * s + 3]),
-                             pack_bf16x2(p[8 * s + 4], p[8 * s + 5]), pack_bf16x2(p[8 * s + 6], p[8 * s + 7]));
+        u32x4 w = u32x4{pack_bf16x2(p[8 * s + 0], p[8 * s + 1]), pack_bf16x2(p[8 * s + 2], p[8 * s + 3]),
+                        pack_bf16x2(p[8 * s + 4], p[8 * s + 5]), pack_bf16x2(p[8 * s + 6], p[8 * s + 7])};
         pb[kb][s] = __builtin_bit_cast(bf16x8, w);
       }
     }
@@ -252,9 +256,9 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
           const int g = 8 * kb + 4 * s + hf;      // keys 4g..4g+3, then 4(g+2)..+3
-          const uint2 lo = *reinterpret_cast<const uint2*>(&lds_v[buf][(g * DH + d) * 4]);
-          const uint2 hi = *reinterpret_cast<const uint2*>(&lds_v[buf][((g + 2) * DH + d) * 4]);
-          bf16x8 va = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+          const u32x2 lo = *reinterpret_cast<const u32x2*>(&lds_v[buf][(g * DH + d) * 4]);
+          const u32x2 hi = *reinterpret_cast<const u32x2*>(&lds_v[buf][((g + 2) * DH + d) * 4]);
+          bf16x8 va = __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, hi.x, hi.y});
           acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kb][s], acc_o[db], 0, 0, 0);
         }
     }
@@ -272,9 +276,9 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
     for (int db = 0; db < DH / 32; ++db)
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
-        const uint2 w = make_uint2(pack_bf16x2(acc_o[db][4 * g4 + 0] * inv, acc_o[db][4 * g4 + 1] * inv),
-                                   pack_bf16x2(acc_o[db][4 * g4 + 2] * inv, acc_o[db][4 * g4 + 3] * inv));
-        *reinterpret_cast<uint2*>(op + db * 32 + 8 * g4) = w;
+        const u32x2 w = u32x2{pack_bf16x2(acc_o[db][4 * g4 + 0] * inv, acc_o[db][4 * g4 + 1] * inv),
+                              pack_bf16x2(acc_o[db][4 * g4 + 2] * inv, acc_o[db][4 * g4 + 3] * inv)};
+        *reinterpret_cast<u32x2*>(op + db * 32 + 8 * g4) = w;
       }
     if (a.lse && hf == 0)
       a.lse[((long long)i * a.H + h) * a.S + qi] = m_run * 0.69314718055994531f + logf(l_tot);
@@ -299,8 +303,10 @@ cast_status_t launch_anchor_attn(const void* q, const void* k_hist, const void* 
   a.k = static_cast<const uint16_t*>(k_hist);
   a.v = static_cast<const uint16_t*>(v_hist);
   a.idx = k_eff > 0 ? idx : nullptr;
-  a.kc = static_cast<const uint16_t*>(k_cur);
-  a.vc = static_cast<const uint16_t*>(v_cur);
+  // keep every base pointer valid even for an empty segment (never dereferenced then)
+  a.kc = static_cast<const uint16_t*>(n0 > 0 ? k_cur : k_hist);
+  a.vc = static_cast<const uint16_t*>(n0 > 0 ? v_cur : v_hist);
+  if (k_eff == 0) { a.k = a.kc; a.v = a.vc; }
   a.out = static_cast<uint16_t*>(out);
   a.lse = lse_out;
   a.n_a = n_a;

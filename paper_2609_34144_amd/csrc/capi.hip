@@ -116,6 +116,8 @@ cast_status_t cast_anchor_attn(const void* q, const void* k_hist, const void* v_
     return fail(CAST_ERR_SHAPE, "attn: need n_a,S,H,Bv>=1 and M,n0,k_eff>=0");
   if (!dh_ok(dh)) return fail(CAST_ERR_UNSUPPORTED, "attn: dh must be 32, 64 or 128 (got %d)", dh);
   if (k_eff > M) return fail(CAST_ERR_SHAPE, "attn: k_eff=%d exceeds M=%d", k_eff, M);
+  if (k_eff > kAttnMaxKeff)
+    return fail(CAST_ERR_UNSUPPORTED, "attn: k_eff=%d exceeds %d routed chunks", k_eff, kAttnMaxKeff);
   long long L = (long long)n0 + (long long)k_eff * Bv;
   if (L < 1) return fail(CAST_ERR_SHAPE, "attn: nothing to attend to (n0 = 0 and k_eff = 0)");
   if (L * (long long)Bv >= (1LL << 40) || L >= (1LL << 31) || L >= (1LL << 24) * (long long)Bv)

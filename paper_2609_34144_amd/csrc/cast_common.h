@@ -49,6 +49,7 @@ cast_status_t launch_route(const void* q, const void* k, int n_a, int S, int H, 
 // ---------------------------------------------------------------------------
 // Attention
 // ---------------------------------------------------------------------------
+constexpr int kAttnMaxKeff = 1024;   // routed chunks per (anchor, head)
 cast_status_t launch_anchor_attn(const void* q, const void* k_hist, const void* v_hist,
                                  const int32_t* idx, int k_eff, const void* k_cur,
                                  const void* v_cur, int n0, int n_a, int S, int H, int dh, int M,

@@ -178,9 +178,15 @@ __global__ __launch_bounds__(64) void par_xspec_kernel(ParArgs a, TileClass k,
   __syncthreads();
   float* dst = partial + (((long long)pair * a.n_tiles + tile) * a.n_chblk + chb) * kVals;
   for (int v = lane; v < kVals; v += kChb) {
-    float s = 0.0f;
-    for (int l = 0; l < kChb; ++l) s += lds[l * kLdsStride + v];
-    dst[v] = s;
+    float s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
+#pragma unroll 16
+    for (int l = 0; l < kChb; l += 4) {
+      s0 += lds[(l + 0) * kLdsStride + v];
+      s1 += lds[(l + 1) * kLdsStride + v];
+      s2 += lds[(l + 2) * kLdsStride + v];
+      s3 += lds[(l + 3) * kLdsStride + v];
+    }
+    dst[v] = (s0 + s1) + (s2 + s3);
   }
 }
 
@@ -223,6 +229,7 @@ __global__ __launch_bounds__(64) void par_gate_kernel(ParArgs a, const float* __
   if (active) {
     const float* src = partial + ((long long)pair * a.n_tiles + tile) * a.n_chblk * kVals +
                        (sky * kNkx + kx) * 3;
+#pragma unroll 8
     for (int j = 0; j < a.n_chblk; ++j) {
       zr += src[(long long)j * kVals + 0];
       zi += src[(long long)j * kVals + 1];
@@ -297,12 +304,28 @@ __global__ __launch_bounds__(64) void par_gate_kernel(ParArgs a, const float* __
 // ---------------------------------------------------------------------------
 // par_recon
 // ---------------------------------------------------------------------------
+// Number of unique stored bins of an HP x WP tile (Hermitian columns keep ky <= HP/2).
+template <int HP, int WP>
+constexpr int unique_bins() {
+  int n = 0;
+  for (int kx = 0; kx <= WP / 2; ++kx) n += col_rows(kx, HP, WP);
+  return n;
+}
+// Slot of unique bin (ky, kx) in that enumeration (column-major over kx).
+template <int HP, int WP>
+constexpr int unique_slot(int ky, int kx) {
+  int n = 0;
+  for (int c = 0; c < kx; ++c) n += col_rows(c, HP, WP);
+  return n + ky;
+}
+
 template <int HP, int WP, bool ACC>
 __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __restrict__ resid,
                                            float* __restrict__ out,
                                            const float4* __restrict__ coef, const TileGeom& g,
-                                           int tile, int c_lane, int pair) {
+                                           int tile, int c_lane, int pair, float* fb_lds) {
   constexpr int NKX = WP / 2 + 1;
+  constexpr int NU = unique_bins<HP, WP>();
   // Lanes past the last channel mirror channel D-1: same inputs, same results, and
   // they sit in the same wave as the lane that owns D-1, so their stores (and
   // read-modify-writes) coincide with it instruction by instruction.
@@ -310,9 +333,24 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
   const long long off = ((long long)g.y0 * a.Wg + g.x0) * a.D;
   const unsigned WgD = (unsigned)(a.Wg * a.D), D = (unsigned)a.D;
   const int fa = a.anchors[pair], fb = a.anchors[pair + 1];
-  float ar[HP][NKX], ai[HP][NKX], br[HP][NKX], bi[HP][NKX];
+  float ar[HP][NKX], ai[HP][NKX];
+  {
+    // F_b is parked in this lane's LDS column (LDS as extra per-lane storage: no
+    // other lane reads it, so no barrier is needed)
+    float br[HP][NKX], bi[HP][NKX];
+    load_fwd<HP, WP>(resid + (long long)fb * a.frame_elems + off, WgD, D, c, br, bi);
+    fft::static_for<0, NKX>([&](auto kk) {
+      constexpr int kx = decltype(kk)::value;
+      fft::static_for<0, col_rows(kx, HP, WP)>([&](auto yy) {
+        constexpr int ky = decltype(yy)::value;
+        constexpr int u = unique_slot<HP, WP>(ky, kx);
+        fb_lds[(2 * u) * kChb] = br[ky][kx];
+        fb_lds[(2 * u + 1) * kChb] = bi[ky][kx];
+      });
+    });
+  }
   load_fwd<HP, WP>(resid + (long long)fa * a.frame_elems + off, WgD, D, c, ar, ai);
-  load_fwd<HP, WP>(resid + (long long)fb * a.frame_elems + off, WgD, D, c, br, bi);
+  (void)NU;
   const int n_pairs = a.n_anchor - 1;
   for (int part = 0; part < 3; ++part) {
     int t0, t1;
@@ -321,21 +359,45 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
     else { if (pair != n_pairs - 1) continue; t0 = fb + 1; t1 = a.n_frames; }
     for (int t = t0; t < t1; ++t) {
       const float4* __restrict__ cf = coef + ((long long)t * a.n_tiles + tile) * kBins;
+      float* dst = out + (long long)t * a.frame_elems + off;   // uniform
+      // Recompute the 64 element offsets per target instead of keeping them live
+      // across the target loop (they would pin 64 VGPRs).
+      unsigned wgd = __builtin_amdgcn_readfirstlane(WgD), dd = __builtin_amdgcn_readfirstlane(D);
+      asm volatile("" : "+s"(wgd), "+s"(dd));
+      // likewise re-read F_b from LDS per target rather than hoisting it into VGPRs
+      const float* fbp = fb_lds;
+      asm volatile("" : "+v"(fbp));
+      // accumulate mode: fetch X_t first, all 64 loads in flight together (nothing
+      // is stored to this frame before they are issued)
+      float old[HP][WP];
+      if constexpr (ACC) {
+        fft::static_for<0, HP>([&](auto yy) {
+          constexpr int y = decltype(yy)::value;
+          fft::static_for<0, WP>([&](auto xx) {
+            constexpr int xi = decltype(xx)::value;
+            old[y][xi] = dst[c + y * wgd + xi * dd];
+          });
+        });
+      }
       // eq:fcpasm blend and the column (y) inverse, one stored column at a time
       float gr[HP][NKX], gi[HP][NKX];
       fft::static_for<0, NKX>([&](auto kk) {
         constexpr int kx = decltype(kk)::value;
+        auto fbr = [&](int u) { return fbp[(2 * u) * kChb]; };
+        auto fbi = [&](int u) { return fbp[(2 * u + 1) * kChb]; };
         if constexpr (herm_col(kx, WP)) {
           float hr[HP / 2 + 1], hi[HP / 2 + 1], col[HP];
           fft::static_for<0, HP / 2 + 1>([&](auto yy) {
             constexpr int ky = decltype(yy)::value;
+            constexpr int u = unique_slot<HP, WP>(ky, kx);
             const float4 k = cf[ky * kNkx + kx];
             if constexpr (self_conj(ky, kx, HP, WP)) {
-              hr[ky] = k.x * ar[ky][kx] + k.z * br[ky][kx];
+              hr[ky] = k.x * ar[ky][kx] + k.z * fbr(u);
               hi[ky] = 0.0f;
             } else {
-              hr[ky] = k.x * ar[ky][kx] - k.y * ai[ky][kx] + k.z * br[ky][kx] - k.w * bi[ky][kx];
-              hi[ky] = k.x * ai[ky][kx] + k.y * ar[ky][kx] + k.z * bi[ky][kx] + k.w * br[ky][kx];
+              const float b_r = fbr(u), b_i = fbi(u);
+              hr[ky] = k.x * ar[ky][kx] - k.y * ai[ky][kx] + k.z * b_r - k.w * b_i;
+              hi[ky] = k.x * ai[ky][kx] + k.y * ar[ky][kx] + k.z * b_i + k.w * b_r;
             }
           });
           fft::c2r<HP>(hr, hi, col);
@@ -348,9 +410,11 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
           float hr[HP], hi[HP];
           fft::static_for<0, HP>([&](auto yy) {
             constexpr int ky = decltype(yy)::value;
+            constexpr int u = unique_slot<HP, WP>(ky, kx);
             const float4 k = cf[ky * kNkx + kx];
-            hr[ky] = k.x * ar[ky][kx] - k.y * ai[ky][kx] + k.z * br[ky][kx] - k.w * bi[ky][kx];
-            hi[ky] = k.x * ai[ky][kx] + k.y * ar[ky][kx] + k.z * bi[ky][kx] + k.w * br[ky][kx];
+            const float b_r = fbr(u), b_i = fbi(u);
+            hr[ky] = k.x * ar[ky][kx] - k.y * ai[ky][kx] + k.z * b_r - k.w * b_i;
+            hi[ky] = k.x * ai[ky][kx] + k.y * ar[ky][kx] + k.z * b_i + k.w * b_r;
           });
           fft::cdft<HP, true>(hr, hi);
           fft::static_for<0, HP>([&](auto yy) {
@@ -361,11 +425,6 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
         }
       });
       // row (x) inverse real transforms and the store / accumulate
-      float* dst = out + (long long)t * a.frame_elems + off;   // uniform
-      // Recompute the 64 element offsets per target instead of keeping them live
-      // across the target loop (they would pin 64 VGPRs).
-      unsigned wgd = __builtin_amdgcn_readfirstlane(WgD), dd = __builtin_amdgcn_readfirstlane(D);
-      asm volatile("" : "+s"(wgd), "+s"(dd));
       fft::static_for<0, HP>([&](auto yy) {
         constexpr int y = decltype(yy)::value;
         float xv[WP];
@@ -373,7 +432,7 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
         fft::static_for<0, WP>([&](auto xx) {
           constexpr int xi = decltype(xx)::value;
           float* p = dst + (c + y * wgd + xi * dd);
-          if constexpr (ACC) *p += xv[xi];
+          if constexpr (ACC) *p = old[y][xi] + xv[xi];
           else __builtin_nontemporal_store(xv[xi], p);
         });
       });
@@ -386,9 +445,11 @@ __global__ __launch_bounds__(64) void par_recon_kernel(ParArgs a, TileClass k,
                                                         const float* __restrict__ resid,
                                                         float* __restrict__ out,
                                                         const float4* __restrict__ coef) {
+  __shared__ float fb_lds[2 * kBins * kChb];
   const int tile = class_tile(a, k, blockIdx.x), chb = blockIdx.y, pair = blockIdx.z;
   const TileGeom g = tile_geom(a, tile);
-  recon_body<HP, WP, ACC>(a, resid, out, coef, g, tile, chb * kChb + threadIdx.x, pair);
+  recon_body<HP, WP, ACC>(a, resid, out, coef, g, tile, chb * kChb + threadIdx.x, pair,
+                          fb_lds + threadIdx.x);
 }
 
 // Host-side table of the per-shape kernels, indexed [HP-1][WP-1].

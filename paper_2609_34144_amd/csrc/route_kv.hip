@@ -78,6 +78,7 @@ __global__ __launch_bounds__(256) void route_finalize_kernel(const float* __rest
   if (seg < n_a) { nsp = spq; first = seg * spq; len = (float)S; }
   else { nsp = spk; first = n_a * spq + (seg - n_a) * spk; len = (float)Bv; }
   float s = 0.0f;
+#pragma unroll 8
   for (int j = 0; j < nsp; ++j) s += partial[(long long)(first + j) * D + c];
   means[(long long)seg * D + c] = s / len;
 }
