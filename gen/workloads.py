@@ -86,7 +86,10 @@ class Workload:
 
     @property
     def frame_tokens(self) -> int:
-        """Current-frame tokens advanced by one block step (N_cur * S)."""
+        """Current-frame tokens advanced by one block step: N_cur * S, or for the
+        PAR-only stress case the reconstructed (skipped) frames' tokens."""
+        if self.kind == "par_only":
+            return (self.n_frames - self.n_a) * self.S
         return self.n_frames * self.S
 
 

@@ -190,7 +190,7 @@ size_t cast_par_workspace_bytes(int n_frames, int n_anchor, int Hg, int Wg, int 
  *          transport phase and gate; entries past a smaller edge tile's bins are 0.
  *          n_tiles = ceil(Hg/tile_h) * ceil(Wg/tile_w), row-major.
  * conf_out fp32 [n_anchor-1, n_tiles] device or NULL: c_p per pair and tile.
- * Sizes: Hg, Wg >= 1; D >= 1; n_frames * Hg * Wg * D < 2^40.
+ * Sizes: Hg, Wg >= 1; D >= 1; one frame Hg * Wg * D < 2^30 elements.
  */
 cast_status_t cast_par_reconstruct(const float* resid, const int* anchors, int n_anchor,
                                    int n_frames, int Hg, int Wg, int D,

@@ -54,7 +54,6 @@ ETA_REL, ETA_ABS, EPS = 1e-6, 1e-8, 1e-8
 
 GATE_PAR, GATE_ONE, GATE_ZERO = 0, 1, 2
 
-
 @dataclass(frozen=True)
 class ParParams:
     """PAR settings; defaults are the paper's (tab:config_cast, App. A.2)."""
@@ -70,7 +69,6 @@ class ParParams:
     gate_mode: int = GATE_PAR   # 0: eq:gate, 1: g == 1 (full transport), 2: g == 0 (linear)
     accumulate: bool = False    # False: out[t] = R_hat_t ; True: out[t] += R_hat_t (eq:block)
 
-
 # ----------------------------------------------------------------------------
 # Tiles and the 2-D real DFT (App. A.2: disjoint tiles, orthonormal, own size)
 # ----------------------------------------------------------------------------
@@ -84,18 +82,15 @@ def tile_starts(n: int, tile: int) -> list[tuple[int, int]]:
         s += tile
     return out
 
-
 def tiles(Hg: int, Wg: int, tile_h: int, tile_w: int) -> list[tuple[int, int, int, int]]:
     """All tiles (y0, Hp, x0, Wp) in row-major tile order."""
     return [(y0, hp, x0, wp) for (y0, hp) in tile_starts(Hg, tile_h)
             for (x0, wp) in tile_starts(Wg, tile_w)]
 
-
 def dft_matrix(n: int, sign: int) -> np.ndarray:
     """E[k, m] = exp(sign * 2 pi i k m / n)."""
     k = np.arange(n)
     return np.exp(sign * 2j * np.pi * np.outer(k, k) / n)
-
 
 def rfft2_ortho(x: np.ndarray) -> np.ndarray:
     """Orthonormal forward 2-D real DFT of x[Hp, Wp, ...] (channels trailing).
@@ -110,7 +105,6 @@ def rfft2_ortho(x: np.ndarray) -> np.ndarray:
     f = np.tensordot(ex, f, axes=(1, 1))                             # [kx, ky, ...]
     return np.swapaxes(f, 0, 1) / math.sqrt(hp * wp)
 
-
 def hermitian_full(f_half: np.ndarray, wp: int) -> np.ndarray:
     """Extend a stored half-spectrum [Hp, Wp//2+1, ...] to [Hp, Wp, ...] using
     F[ky, kx] = conj(F[-ky mod Hp, Wp - kx]) for the columns kx > Wp//2."""
@@ -123,7 +117,6 @@ def hermitian_full(f_half: np.ndarray, wp: int) -> np.ndarray:
             full[ky, kx] = np.conj(f_half[(-ky) % hp, wp - kx])
     return full
 
-
 def irfft2_ortho_complex(f_half: np.ndarray, wp: int) -> np.ndarray:
     """Orthonormal inverse 2-D DFT of the Hermitian-extended spectrum; returns the
     complex result (its imaginary part vanishes when the spectrum is Hermitian)."""
@@ -135,18 +128,15 @@ def irfft2_ortho_complex(f_half: np.ndarray, wp: int) -> np.ndarray:
     r = np.tensordot(ex, r, axes=(1, 1))                             # [x, y, ...]
     return np.swapaxes(r, 0, 1) / math.sqrt(hp * wp)
 
-
 def irfft2_ortho(f_half: np.ndarray, wp: int) -> np.ndarray:
     """Real part of the orthonormal inverse (the inverse real FFT)."""
     return irfft2_ortho_complex(f_half, wp).real
-
 
 # ----------------------------------------------------------------------------
 # Bin bookkeeping (App. A.2: representatives, mirrors, self-conjugate, kappa, nu)
 # ----------------------------------------------------------------------------
 
 REP, MIRROR, SELF = 0, 1, 2
-
 
 def bin_tables(hp: int, wp: int):
     """Per stored bin (ky, kx), ky in [0,Hp), kx in [0, Wp//2]:
@@ -184,14 +174,12 @@ def bin_tables(hp: int, wp: int):
     nu = radius / rmax if rmax > 0 else np.zeros_like(radius)
     return kind, partner, kappa, nu
 
-
 def wrap_arg(z: complex) -> float:
     """Principal argument in (-pi, pi]: atan2, with -pi mapped to +pi."""
     th = math.atan2(z.imag, z.real)
     if th == -math.pi:
         th = math.pi
     return th
-
 
 # ----------------------------------------------------------------------------
 # Per-(pair, tile) statistics: eq:cross, reliability, theta, eq:confidence, eq:gate
@@ -208,13 +196,11 @@ class TileStats:
     nu: np.ndarray        # [Hp, nkx]
     gate: np.ndarray      # [Hp, nkx] g_{p, omega}
 
-
 def cross_spectrum(Fa: np.ndarray, Fb: np.ndarray):
     """eq:cross over the trailing channel axis."""
     Z = (Fb * np.conj(Fa)).sum(axis=-1)
     W = (np.abs(Fb) * np.abs(Fa)).sum(axis=-1)
     return Z, W
-
 
 def tile_stats(Fa: np.ndarray, Fb: np.ndarray, hp: int, wp: int, prm: ParParams) -> TileStats:
     Z, W = cross_spectrum(Fa, Fb)
@@ -254,14 +240,12 @@ def tile_stats(Fa: np.ndarray, Fb: np.ndarray, hp: int, wp: int, prm: ParParams)
     return TileStats(Z=Z, W=W, eta=float(eta), reliable=reliable, theta=theta,
                      conf=conf, nu=nu, gate=gate)
 
-
 def blend(Fa: np.ndarray, Fb: np.ndarray, theta: np.ndarray, gate: np.ndarray,
           alpha: float) -> np.ndarray:
     """eq:fcpasm, per channel (trailing axis), with U^beta = exp(i beta theta)."""
     ua = np.exp(1j * gate * alpha * theta)[..., None]
     ub = np.exp(-1j * gate * (1.0 - alpha) * theta)[..., None]
     return (1.0 - alpha) * Fa * ua + alpha * Fb * ub
-
 
 # ----------------------------------------------------------------------------
 # Composition (eq:block) and the full operator
@@ -295,11 +279,9 @@ def composition(anchors, n_frames: int):
         out.append((t, pa, pb, (t - pa) / (pb - pa)))
     return out
 
-
 def anchor_pairs(anchors):
     a = [int(x) for x in anchors]
     return [(a[j], a[j + 1]) for j in range(len(a) - 1)]
-
 
 def par_stats(resid: np.ndarray, anchors, prm: ParParams = ParParams()):
     """Statistics for every adjacent anchor pair and tile.
@@ -318,7 +300,6 @@ def par_stats(resid: np.ndarray, anchors, prm: ParParams = ParParams()):
         out[(a, b)] = lst
     return out
 
-
 def reconstruct_frame(stats_for_pair, alpha: float, Hg: int, Wg: int, D: int) -> np.ndarray:
     """R_hat_t = P_t(R_a, R_b): blend every tile, inverse-transform, assemble."""
     out = np.zeros((Hg, Wg, D), dtype=np.float64)
@@ -326,7 +307,6 @@ def reconstruct_frame(stats_for_pair, alpha: float, Hg: int, Wg: int, D: int) ->
         Fh = blend(Fa, Fb, st.theta, st.gate, alpha)
         out[y0:y0 + hp, x0:x0 + wp, :] = irfft2_ortho(Fh, wp)
     return out
-
 
 def par_reconstruct(resid: np.ndarray, anchors, prm: ParParams = ParParams(),
                     out: np.ndarray | None = None, targets=None) -> np.ndarray:
@@ -354,6 +334,17 @@ def par_reconstruct(resid: np.ndarray, anchors, prm: ParParams = ParParams(),
             out[t] = r
     return out
 
+def par_reconstruct_targets(resid: np.ndarray, anchors, targets, prm: ParParams = ParParams()):
+    """R_hat_t for the listed skipped frames only, as {t: [Hg, Wg, D] float64}.
+
+    Same arithmetic as par_reconstruct (write mode); reads only the anchor frames
+    of `resid` (which may be float32) and never materialises the full buffer, for
+    sampled checks of large workloads.
+    """
+    n_frames, Hg, Wg, D = resid.shape
+    comp = {t: (a, b, alpha) for (t, a, b, alpha) in composition(anchors, n_frames)}
+    stats = par_stats(resid, anchors, prm)
+    return {t: reconstruct_frame(stats[comp[t][:2]], comp[t][2], Hg, Wg, D) for t in targets}
 
 def stats_arrays(resid: np.ndarray, anchors, prm: ParParams = ParParams()):
     """theta, gate as [n_pairs, n_tiles, tile_h * (tile_w//2 + 1)] and conf as

@@ -30,7 +30,12 @@ def pooled_means(q: np.ndarray, k_hist: np.ndarray):
 def chunk_scores(q: np.ndarray, k_hist: np.ndarray, scale: float = 1.0) -> np.ndarray:
     """eq:pooled scores s[i, h, m] = scale * q_bar[i, h] . k_bar[m, h]."""
     qb, kb = pooled_means(q, k_hist)
-    return scale * np.einsum("ihd,mhd->ihm", qb, kb)
+    return scores_from_means(qb, kb, scale)
+
+
+def scores_from_means(qb: np.ndarray, kb: np.ndarray, scale: float = 1.0) -> np.ndarray:
+    """eq:pooled score from pooled means q_bar [n_a, H, dh] and k_bar [M, H, dh]."""
+    return scale * np.einsum("ihd,mhd->ihm", np.asarray(qb, np.float64), np.asarray(kb, np.float64))
 
 
 def topk_select(scores_1d, topk: int) -> list[int]:

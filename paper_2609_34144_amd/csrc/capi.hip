@@ -168,8 +168,8 @@ static cast_status_t par_shape_check(int n_frames, int n_anchor, int Hg, int Wg,
   if (p->gate_mode < 0 || p->gate_mode > 2) return fail(CAST_ERR_SHAPE, "par: gate_mode must be 0, 1 or 2");
   if (!(p->T > 0.0f) || !(p->q > 0.0f) || !(p->tau_high >= p->tau_low))
     return fail(CAST_ERR_SHAPE, "par: eq:gate needs q > 0, T > 0, tau_high >= tau_low");
-  if ((long long)Hg * Wg * D >= (1LL << 31))
-    return fail(CAST_ERR_UNSUPPORTED, "par: one frame must hold < 2^31 elements");
+  if ((long long)Hg * Wg * D >= (1LL << 30))
+    return fail(CAST_ERR_UNSUPPORTED, "par: one frame must hold < 2^30 elements (4 GiB)");
   return CAST_OK;
 }
 

@@ -71,6 +71,26 @@ __device__ __forceinline__ int class_tile(const ParArgs& a, const TileClass& k, 
   return (k.ty0 + r) * a.n_tx + k.tx0 + (b - r * k.ntx);
 }
 
+// Frame-wide buffer resource: every element access is (lane channel offset in a
+// VGPR) + (token offset, uniform across the wave, in an SGPR); accesses outside
+// the frame return 0 / are dropped by the hardware range check.
+constexpr int kBufDword3 = 0x00020000;   // 32-bit data format, gfx9-family V#
+constexpr int kNT = 2;                   // nontemporal cache policy (streaming stores)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t frame_rsrc(const float* base, long long frame,
+                                                             long long frame_elems) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base) + frame * frame_elems, 0,
+                                           (int)(unsigned)(frame_elems * 4), kBufDword3);
+}
+__device__ __forceinline__ float buf_ld(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
+}
+template <int AUX>
+__device__ __forceinline__ void buf_st(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff,
+                                       float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)voff, (int)soff, AUX);
+}
+
 // A stored column kx holds its own conjugates (kx = 0, and kx = W/2 for even W).
 __host__ __device__ constexpr bool herm_col(int kx, int W) { return kx == 0 || (W % 2 == 0 && 2 * kx == W); }
 // Number of stored rows that are kept for column kx (Hermitian columns keep ky <= H/2).
@@ -81,11 +101,11 @@ __host__ __device__ constexpr bool self_conj(int ky, int kx, int H, int W) {
 
 // Unnormalised forward 2-D real DFT of one channel of one tile, kept on the
 // unique bins only: Hermitian columns ky <= HP/2, other columns all ky.
-// `tile` is the wave-uniform address of channel 0 of the tile's top-left token;
-// `c` is the lane's channel (always in range).
+// `r` covers the frame, `tile0` is the byte offset of channel 0 of the tile's
+// top-left token, `c4` the lane's channel byte offset (always in range).
 template <int HP, int WP>
-__device__ __forceinline__ void load_fwd(const float* __restrict__ tile, unsigned WgD, unsigned D,
-                                         unsigned c, float (&fr)[HP][WP / 2 + 1],
+__device__ __forceinline__ void load_fwd(__amdgpu_buffer_rsrc_t r, unsigned tile0, unsigned WgD4,
+                                         unsigned D4, unsigned c4, float (&fr)[HP][WP / 2 + 1],
                                          float (&fi)[HP][WP / 2 + 1]) {
   constexpr int NKX = WP / 2 + 1;
   float x[HP][WP];
@@ -93,7 +113,7 @@ __device__ __forceinline__ void load_fwd(const float* __restrict__ tile, unsigne
     constexpr int y = decltype(yy)::value;
     fft::static_for<0, WP>([&](auto xx) {
       constexpr int xi = decltype(xx)::value;
-      x[y][xi] = __builtin_nontemporal_load(tile + (c + y * WgD + xi * D));
+      x[y][xi] = buf_ld(r, c4, tile0 + y * WgD4 + xi * D4);
     });
   });
   float rr[HP][NKX], ri[HP][NKX];
@@ -138,12 +158,12 @@ __device__ __forceinline__ void xspec_body(const ParArgs& a, const float* __rest
                                            float* lds_row) {
   constexpr int NKX = WP / 2 + 1;
   const bool valid = c_lane < a.D;
-  const unsigned c = (unsigned)(valid ? c_lane : a.D - 1);
-  const long long off = ((long long)g.y0 * a.Wg + g.x0) * a.D;
+  const unsigned c4 = 4u * (unsigned)(valid ? c_lane : a.D - 1);
+  const unsigned tile0 = 4u * (unsigned)((g.y0 * a.Wg + g.x0) * a.D);
+  const unsigned WgD4 = 4u * (unsigned)(a.Wg * a.D), D4 = 4u * (unsigned)a.D;
   float ar[HP][NKX], ai[HP][NKX], br[HP][NKX], bi[HP][NKX];
-  const unsigned WgD = (unsigned)(a.Wg * a.D), D = (unsigned)a.D;
-  load_fwd<HP, WP>(resid + (long long)fa * a.frame_elems + off, WgD, D, c, ar, ai);
-  load_fwd<HP, WP>(resid + (long long)fb * a.frame_elems + off, WgD, D, c, br, bi);
+  load_fwd<HP, WP>(frame_rsrc(resid, fa, a.frame_elems), tile0, WgD4, D4, c4, ar, ai);
+  load_fwd<HP, WP>(frame_rsrc(resid, fb, a.frame_elems), tile0, WgD4, D4, c4, br, bi);
   const float live = valid ? 1.0f : 0.0f;   // lanes past D contribute nothing
   // every slot of the lane's LDS row is written (zeros where no unique bin lives)
   fft::static_for<0, kNkx * HP>([&](auto bb) {
@@ -329,16 +349,16 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
   // Lanes past the last channel mirror channel D-1: same inputs, same results, and
   // they sit in the same wave as the lane that owns D-1, so their stores (and
   // read-modify-writes) coincide with it instruction by instruction.
-  const unsigned c = (unsigned)(c_lane < a.D ? c_lane : a.D - 1);
-  const long long off = ((long long)g.y0 * a.Wg + g.x0) * a.D;
-  const unsigned WgD = (unsigned)(a.Wg * a.D), D = (unsigned)a.D;
+  const unsigned c4 = 4u * (unsigned)(c_lane < a.D ? c_lane : a.D - 1);
+  const unsigned tile0 = 4u * (unsigned)((g.y0 * a.Wg + g.x0) * a.D);
+  const unsigned WgD4 = 4u * (unsigned)(a.Wg * a.D), D4 = 4u * (unsigned)a.D;
   const int fa = a.anchors[pair], fb = a.anchors[pair + 1];
   float ar[HP][NKX], ai[HP][NKX];
   {
     // F_b is parked in this lane's LDS column (LDS as extra per-lane storage: no
     // other lane reads it, so no barrier is needed)
     float br[HP][NKX], bi[HP][NKX];
-    load_fwd<HP, WP>(resid + (long long)fb * a.frame_elems + off, WgD, D, c, br, bi);
+    load_fwd<HP, WP>(frame_rsrc(resid, fb, a.frame_elems), tile0, WgD4, D4, c4, br, bi);
     fft::static_for<0, NKX>([&](auto kk) {
       constexpr int kx = decltype(kk)::value;
       fft::static_for<0, col_rows(kx, HP, WP)>([&](auto yy) {
@@ -349,7 +369,7 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
       });
     });
   }
-  load_fwd<HP, WP>(resid + (long long)fa * a.frame_elems + off, WgD, D, c, ar, ai);
+  load_fwd<HP, WP>(frame_rsrc(resid, fa, a.frame_elems), tile0, WgD4, D4, c4, ar, ai);
   (void)NU;
   const int n_pairs = a.n_anchor - 1;
   for (int part = 0; part < 3; ++part) {
@@ -359,10 +379,10 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
     else { if (pair != n_pairs - 1) continue; t0 = fb + 1; t1 = a.n_frames; }
     for (int t = t0; t < t1; ++t) {
       const float4* __restrict__ cf = coef + ((long long)t * a.n_tiles + tile) * kBins;
-      float* dst = out + (long long)t * a.frame_elems + off;   // uniform
-      // Recompute the 64 element offsets per target instead of keeping them live
-      // across the target loop (they would pin 64 VGPRs).
-      unsigned wgd = __builtin_amdgcn_readfirstlane(WgD), dd = __builtin_amdgcn_readfirstlane(D);
+      const __amdgpu_buffer_rsrc_t dst = frame_rsrc(out, t, a.frame_elems);
+      // Recompute the uniform token offsets per target instead of keeping 64 of them
+      // live across the target loop.
+      unsigned wgd = __builtin_amdgcn_readfirstlane(WgD4), dd = __builtin_amdgcn_readfirstlane(D4);
       asm volatile("" : "+s"(wgd), "+s"(dd));
       // likewise re-read F_b from LDS per target rather than hoisting it into VGPRs
       const float* fbp = fb_lds;
@@ -375,7 +395,7 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
           constexpr int y = decltype(yy)::value;
           fft::static_for<0, WP>([&](auto xx) {
             constexpr int xi = decltype(xx)::value;
-            old[y][xi] = dst[c + y * wgd + xi * dd];
+            old[y][xi] = buf_ld(dst, c4, tile0 + y * wgd + xi * dd);
           });
         });
       }
@@ -431,9 +451,9 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
         fft::c2r<WP>(gr[y], gi[y], xv);
         fft::static_for<0, WP>([&](auto xx) {
           constexpr int xi = decltype(xx)::value;
-          float* p = dst + (c + y * wgd + xi * dd);
-          if constexpr (ACC) *p = old[y][xi] + xv[xi];
-          else __builtin_nontemporal_store(xv[xi], p);
+          const unsigned so = tile0 + y * wgd + xi * dd;
+          if constexpr (ACC) buf_st<0>(dst, c4, so, old[y][xi] + xv[xi]);
+          else buf_st<kNT>(dst, c4, so, xv[xi]);
         });
       });
     }
