@@ -124,7 +124,8 @@ cast_status_t cast_route_kv(const void* q, const void* k_hist,
  * k_cur, v_cur  bf16 [n0, H, dh] device, the always-attended current/text segment;
  *          may be NULL when n0 == 0.
  * n0 >= 0, 0 <= k_eff <= min(M, 1024), n0 + k_eff*Bv >= 1; dh in {32, 64, 128};
- * scale finite and > 0; (n0 + k_eff*Bv) * Bv < 2^40 and n0 + k_eff*Bv < 2^24 * Bv.
+ * scale finite and > 0; (n0 + k_eff*Bv) * Bv < 2^40 and n0 + k_eff*Bv < 2^24 * Bv;
+ * k_hist, v_hist and k_cur, v_cur each smaller than 4 GiB.
  * out      bf16 [n_a, S, H, dh] device (must not alias the inputs).
  * lse_out  fp32 [n_a, H, S] device natural-log sum of exp of the scaled logits,
  *          or NULL to skip.

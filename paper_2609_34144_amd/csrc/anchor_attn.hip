@@ -31,7 +31,6 @@ typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kBQ = 128;   // queries per workgroup
 constexpr int kBK = 64;    // keys per tile
 constexpr int kThreads = 256;
 constexpr int kMaxKeff = kAttnMaxKeff;   // routed chunk indices cached in LDS
@@ -48,6 +47,7 @@ struct AttnArgs {
   int n_a, S, H, M, Bv, n0, k_eff, L, n_qt, nblocks;
   unsigned long long bv_magic;   // ceil(2^40 / Bv): row / Bv = (row * magic) >> 40
   float sl2;                     // scale * log2(e)
+  long long hist_bytes;          // extent of the K/V history tensors
 };
 
 // Block b runs on XCD b % 8; give each XCD a contiguous range of logical blocks.
@@ -73,19 +73,28 @@ __device__ __forceinline__ const uint16_t* row_ptr(const AttnArgs& a, const uint
   return r < a.n0 ? cp : hp;
 }
 
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Two floats -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  // round to nearest even (finite inputs)
-  uint32_t a = __float_as_uint(lo), b = __float_as_uint(hi);
-  a += 0x7fffu + ((a >> 16) & 1u);
-  b += 0x7fffu + ((b >> 16) & 1u);
-  return (a >> 16) | (b & 0xffff0000u);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
+}
+
+constexpr int kBufDword3 = 0x00020000;   // 32-bit data format, gfx9-family V#
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tensor_rsrc(const void* base, long long bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0,
+                                           (int)(unsigned)(bytes < 0xffffffffll ? bytes : 0xffffffffll),
+                                           kBufDword3);
 }
 
 template <int DH>
 struct Tile {
   static constexpr int KSTR = DH + 8;                // padded K row (bf16 elements)
   static constexpr int K_ELEMS = kBK * KSTR;
-  static constexpr int V_ELEMS = kBK * DH;           // [kBK/4][DH][4]
+  static constexpr int VG_STR = DH * 4 + 8;          // one 4-key group: [DH][4] + 16 B pad
+  static constexpr int V_ELEMS = (kBK / 4) * VG_STR;  // [kBK/4][DH][4] with padded groups
   static constexpr int CPR = DH / 8;                 // 16-byte chunks per row
   static constexpr int RPP = kThreads / CPR;         // rows per load pass
   static constexpr int KPASS = kBK / RPP;            // K load passes per tile
@@ -93,12 +102,13 @@ struct Tile {
   static constexpr int VPASS = (VITEMS + kThreads - 1) / kThreads;
 };
 
-template <int DH>
-__global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
+template <int DH, int QB>
+__global__ __launch_bounds__(kThreads, (QB == 1 ? 2 : 1)) void anchor_attn_kernel(AttnArgs a) {
   using T = Tile<DH>;
+  constexpr int BQ = 4 * 32 * QB;   // queries per workgroup: 4 waves x QB blocks of 32
   __shared__ __attribute__((aligned(16))) uint16_t lds_k[2][T::K_ELEMS];
   __shared__ __attribute__((aligned(16))) uint16_t lds_v[2][T::V_ELEMS];
-  __shared__ int sidx[kMaxKeff];
+  __shared__ int sidx[kMaxKeff + 1];
 
   const int logical = xcd_remap(blockIdx.x, a.nblocks);
   const int pair = logical / a.n_qt, qt = logical - pair * a.n_qt;
@@ -106,46 +116,130 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int l32 = lane & 31, hf = lane >> 5;
   // routed chunk indices of this (anchor, head), clamped into [0, M)
+  // (entry k_eff repeats the last one, so a tile's "next slot" always names a real chunk)
   if (a.k_eff > 0) {
     const int32_t* idx_ih = a.idx + ((long long)i * a.H + h) * a.k_eff;
-    for (int j = tid; j < a.k_eff; j += kThreads) {
-      const int c = idx_ih[j];
+    for (int j = tid; j <= a.k_eff; j += kThreads) {
+      const int c = idx_ih[j < a.k_eff ? j : a.k_eff - 1];
       sidx[j] = c < 0 ? 0 : (c >= a.M ? a.M - 1 : c);
     }
-  } else if (tid == 0) {
-    sidx[0] = 0;
+  } else if (tid < 2) {
+    sidx[tid] = 0;
   }
 
-  // ---- Q^T operand in registers: lane holds query l32, d = 16t + 8hf .. +8
-  const int qi = qt * kBQ + wave * 32 + l32;
-  bf16x8 qreg[DH / 16];
-  {
+  // ---- Q^T operands in registers: for query block qb the lane holds query
+  //      qt*BQ + (wave*QB + qb)*32 + l32, d = 16t + 8hf .. +8
+  bf16x8 qreg[QB][DH / 16];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int qi = qt * BQ + (wave * QB + qb) * 32 + l32;
     // rows past S load the last query; their outputs are never stored
     const int qc = qi < a.S ? qi : a.S - 1;
     const uint16_t* qp = a.q + (((long long)i * a.S + qc) * a.H + h) * DH + 8 * hf;
 #pragma unroll
     for (int t = 0; t < DH / 16; ++t)
-      qreg[t] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qp + 16 * t));
+      qreg[qb][t] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qp + 16 * t));
   }
   __syncthreads();   // sidx visible to every wave
 
   // ---- tile loaders (global -> registers -> LDS)
+  // Row j of tile `tile` is sequence row r = 64*tile + j: current segment rows
+  // r < n0, then routed chunk rows.  When chunks hold >= 64 rows a tile meets at
+  // most two chunks; their slots and indices are wave-uniform, so a lane's row
+  // offset costs a handful of 32-bit ops.  Rows past the end are clamped to the
+  // last row (their logits are masked to -inf and add nothing).
+  const __amdgpu_buffer_rsrc_t rk = tensor_rsrc(a.k, a.hist_bytes);
+  const __amdgpu_buffer_rsrc_t rv = tensor_rsrc(a.v, a.hist_bytes);
+  const unsigned row_bytes = (unsigned)(a.H * DH * 2), head_bytes = (unsigned)(h * DH * 2);
+  // History-only tiles (tile * 64 >= n0): with chunks of >= 64 rows a tile meets at
+  // most two consecutive routed slots s0, s0 + 1, and rows are contiguous inside a
+  // chunk, so row j of the tile sits at (j < split ? base0 : base1) + j * row_bytes
+  // with wave-uniform base0, base1, split.  Rows past the end are harmless: they
+  // read real rows of a routed chunk (sidx is padded) and their logits are masked.
+  struct TileMap { unsigned base0, base1; int split; };
+  auto tile_map = [&](int tile) __attribute__((always_inline)) -> TileMap {
+    const int u0 = tile * kBK - a.n0;                     // first chunk-part row of the tile
+    const int s0 = u0 / a.Bv, tb = s0 * a.Bv;
+    const int c0 = __builtin_amdgcn_readfirstlane(sidx[s0]);
+    const int c1 = __builtin_amdgcn_readfirstlane(sidx[s0 + 1]);
+    TileMap m;
+    m.base0 = (unsigned)(c0 * a.Bv + (u0 - tb)) * row_bytes + head_bytes;
+    m.base1 = (unsigned)(c1 * a.Bv + (u0 - tb - a.Bv)) * row_bytes + head_bytes;
+    m.split = tb + a.Bv - u0;
+    return m;
+  };
+  // general fallback (chunks shorter than a tile): per-row slot by multiply-shift
+  auto hist_off_general = [&](int tile, int j) __attribute__((always_inline)) -> unsigned {
+    int r = tile * kBK + j;
+    r = r < a.L ? r : a.L - 1;
+    const int rr = r - a.n0;
+    const int slot = (int)(((unsigned long long)(unsigned)rr * a.bv_magic) >> 40);
+    const int t = rr - slot * a.Bv;
+    return (unsigned)(sidx[slot] * a.Bv + t) * row_bytes + head_bytes;
+  };
   u32x4 kbuf[T::KPASS];
   u32x4 vbuf[T::VPASS][4];
+  // V items: 16 four-key groups x CPR 16-byte chunks; within a wave, lanes vary the
+  // group fastest (g = lane & 3) so the transposed LDS stores hit distinct banks
+  auto v_item = [&](int it, int& g, int& ch) __attribute__((always_inline)) {
+    g = (it & 3) + 4 * (it / (4 * T::CPR));
+    ch = (it >> 2) % T::CPR;
+  };
   auto load_tile = [&](int tile) __attribute__((always_inline)) {
-    const int r0 = tile * kBK;
+    if (tile * kBK >= a.n0 && a.Bv >= kBK) {
+      // history-only tile, chunks of >= 64 rows: buffer loads, 3 ops per row address
+      const TileMap m = tile_map(tile);
 #pragma unroll
-    for (int p = 0; p < T::KPASS; ++p)
-      kbuf[p] = *reinterpret_cast<const u32x4*>(
-          row_ptr<DH>(a, a.k, a.kc, sidx, r0 + p * T::RPP + tid / T::CPR, h) + (tid % T::CPR) * 8);
+      for (int p = 0; p < T::KPASS; ++p) {
+        const int j = p * T::RPP + tid / T::CPR;
+        const unsigned off = (j < m.split ? m.base0 : m.base1) + (unsigned)j * row_bytes +
+                             (tid % T::CPR) * 16;
+        kbuf[p] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, (int)off, 0, 0));
+      }
 #pragma unroll
-    for (int p = 0; p < T::VPASS; ++p) {
-      const int it = min(tid + p * kThreads, T::VITEMS - 1);
-      const int g = it / T::CPR, ch = it % T::CPR;
+      for (int p = 0; p < T::VPASS; ++p) {
+        int g, ch;
+        v_item(min(tid + p * kThreads, T::VITEMS - 1), g, ch);
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-        vbuf[p][kk] = *reinterpret_cast<const u32x4*>(
-            row_ptr<DH>(a, a.v, a.vc, sidx, r0 + 4 * g + kk, h) + ch * 8);
+        for (int kk = 0; kk < 4; ++kk) {
+          const int j = 4 * g + kk;
+          const unsigned off = (j < m.split ? m.base0 : m.base1) + (unsigned)j * row_bytes + ch * 16;
+          vbuf[p][kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, (int)off, 0, 0));
+        }
+      }
+    } else if (tile * kBK >= a.n0) {
+      // history-only tile, short chunks
+#pragma unroll
+      for (int p = 0; p < T::KPASS; ++p) {
+        const unsigned off = hist_off_general(tile, p * T::RPP + tid / T::CPR) + (tid % T::CPR) * 16;
+        kbuf[p] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, (int)off, 0, 0));
+      }
+#pragma unroll
+      for (int p = 0; p < T::VPASS; ++p) {
+        int g, ch;
+        v_item(min(tid + p * kThreads, T::VITEMS - 1), g, ch);
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          const unsigned off = hist_off_general(tile, 4 * g + kk) + ch * 16;
+          vbuf[p][kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, (int)off, 0, 0));
+        }
+      }
+    } else {
+      // tiles that touch the always-attended current segment: general row addresses
+#pragma unroll
+      for (int p = 0; p < T::KPASS; ++p)
+        kbuf[p] = *reinterpret_cast<const u32x4*>(
+            row_ptr<DH>(a, a.k, a.kc, sidx, tile * kBK + p * T::RPP + tid / T::CPR, h) +
+            (tid % T::CPR) * 8);
+#pragma unroll
+      for (int p = 0; p < T::VPASS; ++p) {
+        int g, ch;
+        v_item(min(tid + p * kThreads, T::VITEMS - 1), g, ch);
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+          vbuf[p][kk] = *reinterpret_cast<const u32x4*>(
+              row_ptr<DH>(a, a.v, a.vc, sidx, tile * kBK + 4 * g + kk, h) + ch * 8);
+      }
     }
   };
   auto store_tile = [&](int buf) __attribute__((always_inline)) {
@@ -158,9 +252,10 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
     for (int p = 0; p < T::VPASS; ++p) {
       const int it = tid + p * kThreads;
       if (it < T::VITEMS) {
-        const int g = it / T::CPR, ch = it % T::CPR;
+        int g, ch;
+        v_item(it, g, ch);
         const u32x4 v0 = vbuf[p][0], v1 = vbuf[p][1], v2 = vbuf[p][2], v3 = vbuf[p][3];
-        u32x4* dst = reinterpret_cast<u32x4*>(&lds_v[buf][(g * DH + ch * 8) * 4]);
+        u32x4* dst = reinterpret_cast<u32x4*>(&lds_v[buf][g * T::VG_STR + ch * 8 * 4]);
         // word w of a row holds d = 8ch + 2w (low half) and 8ch + 2w + 1 (high half);
         // the LDS copy wants, per d, the 4 keys 4g..4g+3 side by side
 #define CAST_VT(w)                                                                   \
@@ -174,12 +269,16 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
     }
   };
 
-  f32x16 acc_o[DH / 32];
+  f32x16 acc_o[QB][DH / 32];
 #pragma unroll
-  for (int db = 0; db < DH / 32; ++db)
+  for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) acc_o[db][e] = 0.0f;
-  float m_run = -INFINITY, l_run = 0.0f;
+    for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc_o[qb][db][e] = 0.0f;
+  float m_run[QB], l_run[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) { m_run[qb] = -INFINITY; l_run[qb] = 0.0f; }
 
   const int ntiles = (a.L + kBK - 1) / kBK;
   load_tile(0);
@@ -190,64 +289,82 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
     const int buf = tile & 1;
     if (tile + 1 < ntiles) load_tile(tile + 1);
 
-    // ---- S^T = K Q^T for the 64 keys of this tile (two 32-key blocks)
-    f32x16 acc_s[2];
+    // ---- S^T = K Q^T for the 64 keys of this tile: each K operand read from LDS
+    //      feeds all QB query blocks
+    f32x16 acc_s[QB][2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc_s[kb][e] = 0.0f;
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc_s[qb][kb][e] = 0.0f;
       const uint16_t* kr = &lds_k[buf][(kb * 32 + l32) * T::KSTR + 8 * hf];
 #pragma unroll
       for (int t = 0; t < DH / 16; ++t) {
         bf16x8 ka = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kr + 16 * t));
-        acc_s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[t], acc_s[kb], 0, 0, 0);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+          acc_s[qb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[qb][t], acc_s[qb][kb], 0, 0, 0);
       }
     }
     // mask keys past the end of the sequence (last tile only)
     const int key0 = tile * kBK;
     if (key0 + kBK > a.L) {
 #pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int key = key0 + kb * 32 + 8 * (e / 4) + 4 * hf + (e % 4);
+            if (key >= a.L) acc_s[qb][kb][e] = -INFINITY;
+          }
+    }
+    // ---- online softmax (log2 domain), one query per lane column
+    bf16x8 pb[QB][2][2];
+    float corr[QB];
+    bool grew = false;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float mx = -INFINITY;
+#pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
+        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc_s[qb][kb][e]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run[qb], mx * a.sl2);
+      grew |= m_new > m_run[qb];
+      corr[qb] = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
+      float rs = 0.0f;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        float p[16];
+#pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const int key = key0 + kb * 32 + 8 * (e / 4) + 4 * hf + (e % 4);
-          if (key >= a.L) acc_s[kb][e] = -INFINITY;
+          p[e] = __builtin_amdgcn_exp2f(fmaf(acc_s[qb][kb][e], a.sl2, -m_new));
+          rs += p[e];
         }
-    }
-    // ---- online softmax (log2 domain)
-    float mx = -INFINITY;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc_s[kb][e]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx * a.sl2);
-    const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
-    float rs = 0.0f;
-    bf16x8 pb[2][2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      float p[16];
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        p[e] = __builtin_amdgcn_exp2f(fmaf(acc_s[kb][e], a.sl2, -m_new));
-        rs += p[e];
+        for (int s = 0; s < 2; ++s) {
+          u32x4 w = u32x4{pack_bf16x2(p[8 * s + 0], p[8 * s + 1]), pack_bf16x2(p[8 * s + 2], p[8 * s + 3]),
+                          pack_bf16x2(p[8 * s + 4], p[8 * s + 5]), pack_bf16x2(p[8 * s + 6], p[8 * s + 7])};
+          pb[qb][kb][s] = __builtin_bit_cast(bf16x8, w);
+        }
       }
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        u32x4 w = u32x4{pack_bf16x2(p[8 * s + 0], p[8 * s + 1]), pack_bf16x2(p[8 * s + 2], p[8 * s + 3]),
-                        pack_bf16x2(p[8 * s + 4], p[8 * s + 5]), pack_bf16x2(p[8 * s + 6], p[8 * s + 7])};
-        pb[kb][s] = __builtin_bit_cast(bf16x8, w);
-      }
+      l_run[qb] = l_run[qb] * corr[qb] + rs;
+      m_run[qb] = m_new;
     }
-    l_run = l_run * corr + rs;
-    m_run = m_new;
+    // rescale O only when some lane's running max moved (wave-uniform branch)
+    if (__ballot(grew) != 0ull) {
 #pragma unroll
-    for (int db = 0; db < DH / 32; ++db)
+      for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc_o[db][e] *= corr;
+        for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc_o[qb][db][e] *= corr[qb];
+    }
 
-    // ---- O^T += V^T P^T
+    // ---- O^T += V^T P^T: each V^T operand read from LDS feeds all QB query blocks
 #pragma unroll
     for (int db = 0; db < DH / 32; ++db) {
       const int d = db * 32 + l32;
@@ -256,10 +373,12 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
           const int g = 8 * kb + 4 * s + hf;      // keys 4g..4g+3, then 4(g+2)..+3
-          const u32x2 lo = *reinterpret_cast<const u32x2*>(&lds_v[buf][(g * DH + d) * 4]);
-          const u32x2 hi = *reinterpret_cast<const u32x2*>(&lds_v[buf][((g + 2) * DH + d) * 4]);
+          const u32x2 lo = *reinterpret_cast<const u32x2*>(&lds_v[buf][g * T::VG_STR + d * 4]);
+          const u32x2 hi = *reinterpret_cast<const u32x2*>(&lds_v[buf][(g + 2) * T::VG_STR + d * 4]);
           bf16x8 va = __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, hi.x, hi.y});
-          acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kb][s], acc_o[db], 0, 0, 0);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb)
+            acc_o[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[qb][kb][s], acc_o[qb][db], 0, 0, 0);
         }
     }
 
@@ -268,26 +387,32 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
   }
 
   // ---- epilogue: normalise, write O (bf16) and the log-sum-exp
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
-  const float inv = 1.0f / l_tot;
-  if (qi < a.S) {
-    uint16_t* op = a.out + (((long long)i * a.S + qi) * a.H + h) * DH + 4 * hf;
 #pragma unroll
-    for (int db = 0; db < DH / 32; ++db)
+  for (int qb = 0; qb < QB; ++qb) {
+    const int qi = qt * BQ + (wave * QB + qb) * 32 + l32;
+    const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
+    const float inv = 1.0f / l_tot;
+    if (qi < a.S) {
+      uint16_t* op = a.out + (((long long)i * a.S + qi) * a.H + h) * DH + 4 * hf;
 #pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const u32x2 w = u32x2{pack_bf16x2(acc_o[db][4 * g4 + 0] * inv, acc_o[db][4 * g4 + 1] * inv),
-                              pack_bf16x2(acc_o[db][4 * g4 + 2] * inv, acc_o[db][4 * g4 + 3] * inv)};
-        *reinterpret_cast<u32x2*>(op + db * 32 + 8 * g4) = w;
-      }
-    if (a.lse && hf == 0)
-      a.lse[((long long)i * a.H + h) * a.S + qi] = m_run * 0.69314718055994531f + logf(l_tot);
+      for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const u32x2 w = u32x2{pack_bf16x2(acc_o[qb][db][4 * g4 + 0] * inv, acc_o[qb][db][4 * g4 + 1] * inv),
+                                pack_bf16x2(acc_o[qb][db][4 * g4 + 2] * inv, acc_o[qb][db][4 * g4 + 3] * inv)};
+          *reinterpret_cast<u32x2*>(op + db * 32 + 8 * g4) = w;
+        }
+      if (a.lse && hf == 0)
+        a.lse[((long long)i * a.H + h) * a.S + qi] = m_run[qb] * 0.69314718055994531f + logf(l_tot);
+    }
   }
 }
 
-template <int DH>
-cast_status_t launch_dh(const AttnArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL(anchor_attn_kernel<DH>, dim3(a.nblocks), dim3(kThreads), 0, stream, a);
+template <int DH, int QB>
+cast_status_t launch_dh(AttnArgs a, hipStream_t stream) {
+  a.n_qt = (a.S + 4 * 32 * QB - 1) / (4 * 32 * QB);
+  a.nblocks = a.n_a * a.H * a.n_qt;
+  hipLaunchKernelGGL((anchor_attn_kernel<DH, QB>), dim3(a.nblocks), dim3(kThreads), 0, stream, a);
   return check_launch("anchor_attn");
 }
 
@@ -317,14 +442,13 @@ cast_status_t launch_anchor_attn(const void* q, const void* k_hist, const void* 
   a.n0 = n0;
   a.k_eff = k_eff;
   a.L = n0 + k_eff * Bv;
-  a.n_qt = (S + kBQ - 1) / kBQ;
-  a.nblocks = n_a * H * a.n_qt;
   a.bv_magic = ((1ull << 40) + (unsigned long long)Bv - 1) / (unsigned long long)Bv;
   a.sl2 = scale * 1.4426950408889634f;
+  a.hist_bytes = k_eff > 0 ? (long long)M * Bv * H * dh * 2 : 0;
   switch (dh) {
-    case 32: return launch_dh<32>(a, stream);
-    case 64: return launch_dh<64>(a, stream);
-    case 128: return launch_dh<128>(a, stream);
+    case 32: return launch_dh<32, 1>(a, stream);
+    case 64: return launch_dh<64, 1>(a, stream);
+    case 128: return launch_dh<128, 1>(a, stream);
     default: return fail(CAST_ERR_UNSUPPORTED, "attn: dh %d", dh);
   }
 }

@@ -126,6 +126,8 @@ cast_status_t cast_anchor_attn(const void* q, const void* k_hist, const void* v_
     return fail(CAST_ERR_SHAPE, "attn: scale must be finite and > 0");
   if ((long long)M * Bv >= (1LL << 31) || (long long)n_a * S >= (1LL << 31))
     return fail(CAST_ERR_UNSUPPORTED, "attn: token counts must stay below 2^31");
+  if ((long long)M * Bv * H * dh * 2 >= (1LL << 32) || (long long)n0 * H * dh * 2 >= (1LL << 32))
+    return fail(CAST_ERR_UNSUPPORTED, "attn: K/V history and current tensors must each be < 4 GiB");
   if (q == nullptr || out == nullptr) return fail(CAST_ERR_NULL, "attn: q and out are required");
   if (k_eff > 0 && (k_hist == nullptr || v_hist == nullptr || idx == nullptr))
     return fail(CAST_ERR_NULL, "attn: k_hist, v_hist and idx are required when k_eff > 0");
