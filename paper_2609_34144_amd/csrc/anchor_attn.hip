@@ -4,19 +4,27 @@
 // online softmax.  One workgroup = 4 waves = 128 queries of one (anchor, head);
 // each wave owns 32 queries.  The key sequence of the (anchor, head) is the
 // concatenation [current segment (n0 tokens) ; routed chunk idx[0] ; ... ], walked
-// in tiles of 64 keys; each tile's rows are gathered from their chunk by index
-// into LDS (double-buffered, one barrier per tile).
+// in tiles of 64 keys.
 //
-// Layout choices (per wave, per 64-key tile):
-//   S^T = K Q^T   A = K tile from LDS (row-major, padded rows), B = Q^T held in
-//                 registers for the whole kernel.  The 32x32 accumulator puts one
-//                 query per lane column, so the row max / row sum of the online
-//                 softmax need only the lane's own values and one exchange with
-//                 lane^32.
+// Data movement: every K and V tile is copied global -> LDS by the buffer unit
+// (buffer_load_dwordx4 ... lds), so no registers or VALU work stage it.  Each
+// lane of a copy instruction picks its source row and 16-byte chunk, which lets
+// the LDS image be XOR-swizzled against bank conflicts even though the copy
+// writes 1 KB contiguously.  Two K and two V buffers rotate; one barrier per tile.
+//
+// Per wave and tile:
+//   S^T = K Q^T   A = K rows from LDS (ds_read_b128), B = Q^T held in registers
+//                 for the whole kernel.  The 32x32 accumulator puts one query per
+//                 lane column, so the online-softmax row max / row sum need only
+//                 the lane's own values and one exchange with lane ^ 32.
 //   O^T += V^T P^T  B = P^T straight from the S^T accumulators (converted to
 //                 bf16; the contraction index order is free, so no data moves),
-//                 A = V^T from an LDS copy of the V tile stored as
-//                 [key/4][d][key%4] so each lane reads its 4-key runs as 8 bytes.
+//                 A = V^T read from the row-major V tile with the transposing
+//                 LDS load ds_read_b64_tr_b16.
+// Software pipeline: iteration j issues the copies of K[j+2] and V[j], the
+// MFMAs of S[j+1] = K[j+1] Q^T and of O += P[j-1] V[j-1], and the softmax of S[j]
+// (VALU); the three are independent, so the matrix cores and the VALU overlap
+// inside one wave.
 // Blocks are renumbered so that the Q-tiles of one (anchor, head) land on the
 // same XCD and share its L2 for the routed K/V.
 #include "cast_common.h"
@@ -27,13 +35,22 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef __attribute__((address_space(3))) char lds_char;
 
 constexpr int kBK = 64;    // keys per tile
 constexpr int kThreads = 256;
 constexpr int kMaxKeff = kAttnMaxKeff;   // routed chunk indices cached in LDS
+// The running max used for the exponentials moves only when the tile max exceeds
+// it by more than this (log2 units): probabilities stay <= 2^8, harmless in fp32
+// sums and bf16 operands, and the O rescale is skipped for most tiles.
+constexpr float kMaxSlack = 8.0f;
 
 struct AttnArgs {
   const uint16_t* q;
@@ -48,7 +65,21 @@ struct AttnArgs {
   unsigned long long bv_magic;   // ceil(2^40 / Bv): row / Bv = (row * magic) >> 40
   float sl2;                     // scale * log2(e)
   long long hist_bytes;          // extent of the K/V history tensors
+  long long cur_bytes;           // extent of the current-segment K/V tensors
 };
+
+template <int V>
+struct IC {
+  static constexpr int value = V;
+};
+
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(IC<B>{});
+    static_for<B + 1, E>(f);
+  }
+}
 
 // Block b runs on XCD b % 8; give each XCD a contiguous range of logical blocks.
 __device__ __forceinline__ int xcd_remap(int b, int nb) {
@@ -56,25 +87,6 @@ __device__ __forceinline__ int xcd_remap(int b, int nb) {
   const int xcd = b % 8, j = b / 8;
   return (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + j;
 }
-
-// Address of key/value row r of the (anchor, head) sequence [current ; routed chunks].
-// Rows past the end are clamped to the last row (their logits are masked, so they
-// contribute exactly zero); chunk indices come from the LDS copy `sidx`.
-template <int DH>
-__device__ __forceinline__ const uint16_t* row_ptr(const AttnArgs& a, const uint16_t* hist,
-                                                   const uint16_t* cur, const int* sidx, int r,
-                                                   int h) {
-  r = r < a.L ? r : a.L - 1;
-  const unsigned rr = (unsigned)max(r - a.n0, 0);
-  const unsigned slot = (unsigned)(((unsigned long long)rr * a.bv_magic) >> 40);
-  const unsigned t = rr - slot * (unsigned)a.Bv;
-  const uint16_t* hp = hist + (((long long)sidx[slot] * a.Bv + t) * a.H + h) * DH;
-  const uint16_t* cp = cur + ((long long)r * a.H + h) * DH;
-  return r < a.n0 ? cp : hp;
-}
-
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // Two floats -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -90,30 +102,42 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t tensor_rsrc(const void* base, 
 }
 
 template <int DH>
-struct Tile {
-  static constexpr int KSTR = DH + 8;                // padded K row (bf16 elements)
-  static constexpr int K_ELEMS = kBK * KSTR;
-  static constexpr int VG_STR = DH * 4 + 8;          // one 4-key group: [DH][4] + 16 B pad
-  static constexpr int V_ELEMS = (kBK / 4) * VG_STR;  // [kBK/4][DH][4] with padded groups
-  static constexpr int CPR = DH / 8;                 // 16-byte chunks per row
-  static constexpr int RPP = kThreads / CPR;         // rows per load pass
-  static constexpr int KPASS = kBK / RPP;            // K load passes per tile
-  static constexpr int VITEMS = (kBK / 4) * CPR;     // V items (4 rows x 16 bytes)
-  static constexpr int VPASS = (VITEMS + kThreads - 1) / kThreads;
+struct Geo {
+  static constexpr int CPR = DH / 8;                     // 16-byte chunks per row
+  static constexpr int ROWB = DH * 2;                    // bytes per row
+  static constexpr int TILEB = kBK * ROWB;               // bytes per K or V tile
+  static constexpr int DPT = TILEB / (kThreads * 16);    // copy instructions per thread per tile
 };
 
-template <int DH, int QB>
-__global__ __launch_bounds__(kThreads, (QB == 1 ? 2 : 1)) void anchor_attn_kernel(AttnArgs a) {
-  using T = Tile<DH>;
-  constexpr int BQ = 4 * 32 * QB;   // queries per workgroup: 4 waves x QB blocks of 32
-  __shared__ __attribute__((aligned(16))) uint16_t lds_k[2][T::K_ELEMS];
-  __shared__ __attribute__((aligned(16))) uint16_t lds_v[2][T::V_ELEMS];
+// LDS swizzles (chunk c of tile row r is stored at chunk c ^ swz(r)):
+//  K: a ds_read_b128 of one logical chunk by 32 consecutive rows; XOR by r mod CPR
+//     spreads any 16 consecutive rows over 16 distinct 16-byte bank groups.
+//  V: a transposing read takes 4 consecutive rows x 32 bytes per 16 lanes, the
+//     two 16-lane halves of 32 lanes 32 bytes apart; XOR by {0, 10, 4, 14}[r mod 4]
+//     gives the 8 row segments of 32 lanes 8 distinct 32-byte bank groups.
+__device__ __forceinline__ constexpr int kswz(int r, int cpr) { return r & (cpr - 1); }
+__device__ __forceinline__ constexpr int vswz(int r, int cpr) {
+  return ((2 * (r & 3)) ^ (8 * (r & 1))) & (cpr - 1);
+}
+
+// FAST: no current segment and chunks of >= 64 rows, so every tile takes the
+// uniform two-chunk mapping and its copies can be issued inside the MFMA block.
+template <int DH, bool FAST>
+__global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
+  using G = Geo<DH>;
+  // separate objects, so the compiler can tell the copy targets from the buffers
+  // being read and does not wait for in-flight copies before unrelated LDS reads
+  __shared__ __attribute__((aligned(1024))) uint16_t lds_k0[kBK * DH];
+  __shared__ __attribute__((aligned(1024))) uint16_t lds_k1[kBK * DH];
+  __shared__ __attribute__((aligned(1024))) uint16_t lds_v0[kBK * DH];
+  __shared__ __attribute__((aligned(1024))) uint16_t lds_v1[kBK * DH];
   __shared__ int sidx[kMaxKeff + 1];
 
   const int logical = xcd_remap(blockIdx.x, a.nblocks);
   const int pair = logical / a.n_qt, qt = logical - pair * a.n_qt;
   const int i = pair / a.H, h = pair - (pair / a.H) * a.H;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hf = lane >> 5;
   // routed chunk indices of this (anchor, head), clamped into [0, M)
   // (entry k_eff repeats the last one, so a tile's "next slot" always names a real chunk)
@@ -127,35 +151,48 @@ __global__ __launch_bounds__(kThreads, (QB == 1 ? 2 : 1)) void anchor_attn_kerne
     sidx[tid] = 0;
   }
 
-  // ---- Q^T operands in registers: for query block qb the lane holds query
-  //      qt*BQ + (wave*QB + qb)*32 + l32, d = 16t + 8hf .. +8
-  bf16x8 qreg[QB][DH / 16];
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int qi = qt * BQ + (wave * QB + qb) * 32 + l32;
+  // ---- Q^T operand in registers: the lane holds query qt*128 + wave*32 + l32,
+  //      d = 16t + 8hf .. +8
+  bf16x8 qreg[DH / 16];
+  {
+    const int qi = qt * 128 + wave * 32 + l32;
     // rows past S load the last query; their outputs are never stored
     const int qc = qi < a.S ? qi : a.S - 1;
     const uint16_t* qp = a.q + (((long long)i * a.S + qc) * a.H + h) * DH + 8 * hf;
 #pragma unroll
     for (int t = 0; t < DH / 16; ++t)
-      qreg[qb][t] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qp + 16 * t));
+      qreg[t] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qp + 16 * t));
   }
   __syncthreads();   // sidx visible to every wave
 
-  // ---- tile loaders (global -> registers -> LDS)
-  // Row j of tile `tile` is sequence row r = 64*tile + j: current segment rows
-  // r < n0, then routed chunk rows.  When chunks hold >= 64 rows a tile meets at
-  // most two chunks; their slots and indices are wave-uniform, so a lane's row
-  // offset costs a handful of 32-bit ops.  Rows past the end are clamped to the
-  // last row (their logits are masked to -inf and add nothing).
-  const __amdgpu_buffer_rsrc_t rk = tensor_rsrc(a.k, a.hist_bytes);
-  const __amdgpu_buffer_rsrc_t rv = tensor_rsrc(a.v, a.hist_bytes);
   const unsigned row_bytes = (unsigned)(a.H * DH * 2), head_bytes = (unsigned)(h * DH * 2);
-  // History-only tiles (tile * 64 >= n0): with chunks of >= 64 rows a tile meets at
-  // most two consecutive routed slots s0, s0 + 1, and rows are contiguous inside a
-  // chunk, so row j of the tile sits at (j < split ? base0 : base1) + j * row_bytes
-  // with wave-uniform base0, base1, split.  Rows past the end are harmless: they
-  // read real rows of a routed chunk (sidx is padded) and their logits are masked.
+
+  // ---- copy slots: instruction n of this wave fills LDS chunk
+  //      ci = (wave * DPT + n) * 64 + lane of a tile, i.e. row ci / CPR and
+  //      physical chunk ci % CPR, which holds logical chunk (ci % CPR) ^ swz(row)
+  auto slot_row = [&](int n) __attribute__((always_inline)) -> int {
+    return ((wave * G::DPT + n) * 64 + lane) / G::CPR;
+  };
+  auto slot_off = [&](int n, bool is_v) __attribute__((always_inline)) -> unsigned {
+    const int r = slot_row(n), pc = lane % G::CPR;
+    return (unsigned)((pc ^ (is_v ? vswz(r, G::CPR) : kswz(r, G::CPR))) * 16);
+  };
+  auto copy16 = [&](__amdgpu_buffer_rsrc_t rs, uint16_t* dst, int n, unsigned off)
+      __attribute__((always_inline)) {
+    // recomputed at each use (the laundering stops the compiler from keeping the
+    // 16 LDS bases of all buffers live in scalar registers across the loop)
+    int wbase = wave * G::DPT * 1024;
+    asm volatile("" : "+s"(wbase));
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        rs, (lds_void*)(reinterpret_cast<char*>(dst) + wbase + n * 1024), 16, (int)off, 0, 0, 0);
+  };
+  // Copy tile `tile` of K (IsV = 0) or V (IsV = 1) into `dst`.  Row j of the tile is
+  // sequence row r = 64*tile + j: current segment rows r < n0, then routed chunk
+  // rows.  History-only tiles with chunks of >= 64 rows meet at most two routed
+  // slots s0, s0 + 1, whose rows are contiguous, so row j sits at
+  // (j < split ? base0 : base1) + j * row_bytes with wave-uniform base0, base1,
+  // split.  Rows past the end read real rows (clamped, or of the padded slot);
+  // their logits are masked to -inf and add nothing.
   struct TileMap { unsigned base0, base1; int split; };
   auto tile_map = [&](int tile) __attribute__((always_inline)) -> TileMap {
     const int u0 = tile * kBK - a.n0;                     // first chunk-part row of the tile
@@ -168,229 +205,329 @@ __global__ __launch_bounds__(kThreads, (QB == 1 ? 2 : 1)) void anchor_attn_kerne
     m.split = tb + a.Bv - u0;
     return m;
   };
-  // general fallback (chunks shorter than a tile): per-row slot by multiply-shift
-  auto hist_off_general = [&](int tile, int j) __attribute__((always_inline)) -> unsigned {
-    int r = tile * kBK + j;
-    r = r < a.L ? r : a.L - 1;
-    const int rr = r - a.n0;
-    const int slot = (int)(((unsigned long long)(unsigned)rr * a.bv_magic) >> 40);
-    const int t = rr - slot * a.Bv;
-    return (unsigned)(sidx[slot] * a.Bv + t) * row_bytes + head_bytes;
+  auto copy_fast = [&](auto is_v, const TileMap& m, int n, uint16_t* dst) __attribute__((always_inline)) {
+    constexpr bool IsV = decltype(is_v)::value != 0;
+    const int r = slot_row(n);
+    const unsigned off = (r < m.split ? m.base0 : m.base1) + (unsigned)r * row_bytes + slot_off(n, IsV);
+    copy16(tensor_rsrc(IsV ? a.v : a.k, a.hist_bytes), dst, n, off);
   };
-  u32x4 kbuf[T::KPASS];
-  u32x4 vbuf[T::VPASS][4];
-  // V items: 16 four-key groups x CPR 16-byte chunks; within a wave, lanes vary the
-  // group fastest (g = lane & 3) so the transposed LDS stores hit distinct banks
-  auto v_item = [&](int it, int& g, int& ch) __attribute__((always_inline)) {
-    g = (it & 3) + 4 * (it / (4 * T::CPR));
-    ch = (it >> 2) % T::CPR;
-  };
-  auto load_tile = [&](int tile) __attribute__((always_inline)) {
-    if (tile * kBK >= a.n0 && a.Bv >= kBK) {
-      // history-only tile, chunks of >= 64 rows: buffer loads, 3 ops per row address
+  auto load_tile = [&](auto is_v, int tile, uint16_t* dst) __attribute__((always_inline)) {
+    constexpr bool IsV = decltype(is_v)::value != 0;
+    const __amdgpu_buffer_rsrc_t rh = tensor_rsrc(IsV ? a.v : a.k, a.hist_bytes);
+    if (FAST || (tile * kBK >= a.n0 && a.Bv >= kBK)) {
       const TileMap m = tile_map(tile);
 #pragma unroll
-      for (int p = 0; p < T::KPASS; ++p) {
-        const int j = p * T::RPP + tid / T::CPR;
-        const unsigned off = (j < m.split ? m.base0 : m.base1) + (unsigned)j * row_bytes +
-                             (tid % T::CPR) * 16;
-        kbuf[p] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, (int)off, 0, 0));
-      }
-#pragma unroll
-      for (int p = 0; p < T::VPASS; ++p) {
-        int g, ch;
-        v_item(min(tid + p * kThreads, T::VITEMS - 1), g, ch);
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          const int j = 4 * g + kk;
-          const unsigned off = (j < m.split ? m.base0 : m.base1) + (unsigned)j * row_bytes + ch * 16;
-          vbuf[p][kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, (int)off, 0, 0));
-        }
-      }
-    } else if (tile * kBK >= a.n0) {
-      // history-only tile, short chunks
-#pragma unroll
-      for (int p = 0; p < T::KPASS; ++p) {
-        const unsigned off = hist_off_general(tile, p * T::RPP + tid / T::CPR) + (tid % T::CPR) * 16;
-        kbuf[p] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, (int)off, 0, 0));
-      }
-#pragma unroll
-      for (int p = 0; p < T::VPASS; ++p) {
-        int g, ch;
-        v_item(min(tid + p * kThreads, T::VITEMS - 1), g, ch);
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          const unsigned off = hist_off_general(tile, 4 * g + kk) + ch * 16;
-          vbuf[p][kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, (int)off, 0, 0));
-        }
-      }
+      for (int n = 0; n < G::DPT; ++n) copy_fast(is_v, m, n, dst);
     } else {
-      // tiles that touch the always-attended current segment: general row addresses
+      // tiles that touch the current segment, or chunks shorter than a tile:
+      // per-row slot by multiply-shift
 #pragma unroll
-      for (int p = 0; p < T::KPASS; ++p)
-        kbuf[p] = *reinterpret_cast<const u32x4*>(
-            row_ptr<DH>(a, a.k, a.kc, sidx, tile * kBK + p * T::RPP + tid / T::CPR, h) +
-            (tid % T::CPR) * 8);
-#pragma unroll
-      for (int p = 0; p < T::VPASS; ++p) {
-        int g, ch;
-        v_item(min(tid + p * kThreads, T::VITEMS - 1), g, ch);
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
-          vbuf[p][kk] = *reinterpret_cast<const u32x4*>(
-              row_ptr<DH>(a, a.v, a.vc, sidx, tile * kBK + 4 * g + kk, h) + ch * 8);
-      }
-    }
-  };
-  auto store_tile = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-    for (int p = 0; p < T::KPASS; ++p) {
-      const int row = p * T::RPP + tid / T::CPR;
-      *reinterpret_cast<u32x4*>(&lds_k[buf][row * T::KSTR + (tid % T::CPR) * 8]) = kbuf[p];
-    }
-#pragma unroll
-    for (int p = 0; p < T::VPASS; ++p) {
-      const int it = tid + p * kThreads;
-      if (it < T::VITEMS) {
-        int g, ch;
-        v_item(it, g, ch);
-        const u32x4 v0 = vbuf[p][0], v1 = vbuf[p][1], v2 = vbuf[p][2], v3 = vbuf[p][3];
-        u32x4* dst = reinterpret_cast<u32x4*>(&lds_v[buf][g * T::VG_STR + ch * 8 * 4]);
-        // word w of a row holds d = 8ch + 2w (low half) and 8ch + 2w + 1 (high half);
-        // the LDS copy wants, per d, the 4 keys 4g..4g+3 side by side
-#define CAST_VT(w)                                                                   \
-  dst[w] = u32x4{__builtin_amdgcn_perm(v1[w], v0[w], 0x05040100u),                   \
-                 __builtin_amdgcn_perm(v3[w], v2[w], 0x05040100u),                   \
-                 __builtin_amdgcn_perm(v1[w], v0[w], 0x07060302u),                   \
-                 __builtin_amdgcn_perm(v3[w], v2[w], 0x07060302u)};
-        CAST_VT(0) CAST_VT(1) CAST_VT(2) CAST_VT(3)
-#undef CAST_VT
+      for (int n = 0; n < G::DPT; ++n) {
+        int r = tile * kBK + slot_row(n);
+        r = r < a.L ? r : a.L - 1;
+        const unsigned co = slot_off(n, IsV);
+        const int rr = max(r - a.n0, 0);
+        const int slot = (int)(((unsigned long long)(unsigned)rr * a.bv_magic) >> 40);
+        const int t = rr - slot * a.Bv;
+        const unsigned hoff = (unsigned)(sidx[slot] * a.Bv + t) * row_bytes + head_bytes + co;
+        // two copies under complementary lane masks (not an if/else, which would be
+        // merged into one copy with a per-lane descriptor)
+        if (r < a.n0)
+          copy16(tensor_rsrc(IsV ? a.vc : a.kc, a.cur_bytes), dst, n,
+                 (unsigned)r * row_bytes + head_bytes + co);
+        if (r >= a.n0) copy16(rh, dst, n, hoff);
       }
     }
   };
 
-  f32x16 acc_o[QB][DH / 32];
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-    for (int db = 0; db < DH / 32; ++db)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc_o[qb][db][e] = 0.0f;
-  float m_run[QB], l_run[QB];
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) { m_run[qb] = -INFINITY; l_run[qb] = 0.0f; }
+  // ---- LDS read addresses (bytes within a tile)
+  // K: lane reads row kb*32 + l32, logical chunk 2t + hf, stored at chunk
+  // (2t + hf) ^ (l32 % CPR); as bytes that is kbase ^ 32t (the row offset is a
+  // multiple of the row length, so the XOR only touches the chunk bits)
+  const unsigned kbase = (unsigned)(l32 * G::ROWB + ((hf ^ kswz(l32, G::CPR)) * 16));
+  // V (transposing read): within each 16-lane group gq = lane / 16, lane a supplies
+  // row 4*(gq/2) + a/4 (+ 32kb + 16s + 8run) and columns d = 32db + 16(gq%2) + 4(a%4)
+  // .. +4; the read returns to lane a the 4 rows' values at d = 32db + 16(gq%2) + a,
+  // i.e. to every lane the column d = 32db + l32 for 4 consecutive keys.
+  // As bytes: vbase ^ 64db (the row swizzle of vr only touches the chunk bits).
+  unsigned vbase;
+  {
+    const int gq = lane >> 4, la = lane & 15;
+    const int vr = 4 * (gq >> 1) + (la >> 2);
+    const int c = 2 * (gq & 1) + ((la & 3) >> 1);
+    vbase = (unsigned)(vr * G::ROWB + ((c ^ vswz(vr, G::CPR)) * 16) + 8 * (la & 1));
+  }
 
-  const int ntiles = (a.L + kBK - 1) / kBK;
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
+  f32x16 acc_o[DH / 32];
+#pragma unroll
+  for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc_o[db][e] = 0.0f;
+  float m_run = -INFINITY, l_run = 0.0f;
 
-  for (int tile = 0; tile < ntiles; ++tile) {
-    const int buf = tile & 1;
-    if (tile + 1 < ntiles) load_tile(tile + 1);
-
-    // ---- S^T = K Q^T for the 64 keys of this tile: each K operand read from LDS
-    //      feeds all QB query blocks
-    f32x16 acc_s[QB][2];
+  // S^T = K Q^T for the 64 keys of the tile in `kt`
+  auto qk = [&](const uint16_t* kt, f32x16 (&acc)[2]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
+      for (int e = 0; e < 16; ++e) acc[kb][e] = 0.0f;
+    const char* kb0 = reinterpret_cast<const char*>(kt);
 #pragma unroll
-        for (int e = 0; e < 16; ++e) acc_s[qb][kb][e] = 0.0f;
-      const uint16_t* kr = &lds_k[buf][(kb * 32 + l32) * T::KSTR + 8 * hf];
-#pragma unroll
-      for (int t = 0; t < DH / 16; ++t) {
-        bf16x8 ka = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kr + 16 * t));
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
-          acc_s[qb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[qb][t], acc_s[qb][kb], 0, 0, 0);
-      }
-    }
-    // mask keys past the end of the sequence (last tile only)
-    const int key0 = tile * kBK;
-    if (key0 + kBK > a.L) {
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int key = key0 + kb * 32 + 8 * (e / 4) + 4 * hf + (e % 4);
-            if (key >= a.L) acc_s[qb][kb][e] = -INFINITY;
-          }
-    }
-    // ---- online softmax (log2 domain), one query per lane column
-    bf16x8 pb[QB][2][2];
-    float corr[QB];
-    bool grew = false;
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc_s[qb][kb][e]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run[qb], mx * a.sl2);
-      grew |= m_new > m_run[qb];
-      corr[qb] = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
-      float rs = 0.0f;
+    for (int t = 0; t < DH / 16; ++t)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        float p[16];
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          p[e] = __builtin_amdgcn_exp2f(fmaf(acc_s[qb][kb][e], a.sl2, -m_new));
-          rs += p[e];
-        }
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          u32x4 w = u32x4{pack_bf16x2(p[8 * s + 0], p[8 * s + 1]), pack_bf16x2(p[8 * s + 2], p[8 * s + 3]),
-                          pack_bf16x2(p[8 * s + 4], p[8 * s + 5]), pack_bf16x2(p[8 * s + 6], p[8 * s + 7])};
-          pb[qb][kb][s] = __builtin_bit_cast(bf16x8, w);
-        }
+        const bf16x8 ka = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(kb0 + (kbase ^ (32u * t)) + kb * 32 * G::ROWB));
+        acc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[t], acc[kb], 0, 0, 0);
       }
-      l_run[qb] = l_run[qb] * corr[qb] + rs;
-      m_run[qb] = m_new;
-    }
-    // rescale O only when some lane's running max moved (wave-uniform branch)
-    if (__ballot(grew) != 0ull) {
+  };
+  // O^T += V^T P^T for the tile in `vt`.  MFMA (kb, s) contracts the keys
+  // 32kb + 16s + 4hf + {0..3} and 32kb + 16s + 8 + 4hf + {0..3}: the S^T accumulator
+  // rows that lane holds as p[8s .. 8s+7] of block kb.
+  auto pv = [&](const uint16_t* vt, const bf16x8 (&pb)[2][2]) __attribute__((always_inline)) {
+    const lds_char* vb0 = (const lds_char*)(vt);
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int db = 0; db < DH / 32; ++db)
+      for (int s = 0; s < 2; ++s)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) acc_o[qb][db][e] *= corr[qb];
-    }
-
-    // ---- O^T += V^T P^T: each V^T operand read from LDS feeds all QB query blocks
-#pragma unroll
-    for (int db = 0; db < DH / 32; ++db) {
-      const int d = db * 32 + l32;
+        for (int db = 0; db < DH / 32; ++db) {
+          const lds_char* p = vb0 + (vbase ^ (64u * db)) + (32 * kb + 16 * s) * G::ROWB;
+          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
+          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + 8 * G::ROWB));
+          const bf16x8 va = __builtin_bit_cast(
+              bf16x8, u32x4{__builtin_bit_cast(u32x2, lo).x, __builtin_bit_cast(u32x2, lo).y,
+                            __builtin_bit_cast(u32x2, hi).x, __builtin_bit_cast(u32x2, hi).y});
+          acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kb][s], acc_o[db], 0, 0, 0);
+        }
+  };
+  // online softmax of tile `tile` (log2 domain), one query per lane column
+  auto softmax = [&](f32x16 (&acc)[2], int tile, bf16x8 (&pb)[2][2], float& corr, bool& grew,
+                     auto mask) __attribute__((always_inline)) {
+    const int key0 = tile * kBK;
+    if (decltype(mask)::value) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          const int g = 8 * kb + 4 * s + hf;      // keys 4g..4g+3, then 4(g+2)..+3
-          const u32x2 lo = *reinterpret_cast<const u32x2*>(&lds_v[buf][g * T::VG_STR + d * 4]);
-          const u32x2 hi = *reinterpret_cast<const u32x2*>(&lds_v[buf][(g + 2) * T::VG_STR + d * 4]);
-          bf16x8 va = __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, hi.x, hi.y});
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb)
-            acc_o[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[qb][kb][s], acc_o[qb][db], 0, 0, 0);
+        for (int e = 0; e < 16; ++e) {
+          const int key = key0 + kb * 32 + 8 * (e / 4) + 4 * hf + (e % 4);
+          if (key >= a.L) acc[kb][e] = -INFINITY;
         }
     }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc[kb][e]);
+    {
+      const u32x2 sw = __builtin_bit_cast(
+          u32x2, __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, mx),
+                                                  __builtin_bit_cast(unsigned, mx), false, false));
+      mx = fmaxf(__builtin_bit_cast(float, sw.x), __builtin_bit_cast(float, sw.y));
+    }
+    const float m_cand = fmaxf(m_run, mx * a.sl2);
+    const bool up = m_cand > m_run + kMaxSlack;
+    const float m_new = up ? m_cand : m_run;
+    grew = __ballot(up) != 0ull;
+    corr = __builtin_amdgcn_exp2f(m_run - m_new);
+    float rs = 0.0f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      float p[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        p[e] = __builtin_amdgcn_exp2f(fmaf(acc[kb][e], a.sl2, -m_new));
+        rs += p[e];
+      }
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const u32x4 w = u32x4{pack_bf16x2(p[8 * s + 0], p[8 * s + 1]), pack_bf16x2(p[8 * s + 2], p[8 * s + 3]),
+                              pack_bf16x2(p[8 * s + 4], p[8 * s + 5]), pack_bf16x2(p[8 * s + 6], p[8 * s + 7])};
+        pb[kb][s] = __builtin_bit_cast(bf16x8, w);
+      }
+    }
+    l_run = l_run * corr + rs;
+    m_run = m_new;
+  };
 
-    if (tile + 1 < ntiles) store_tile(buf ^ 1);
-    __syncthreads();
+  const int nt = (a.L + kBK - 1) / kBK;
+  f32x16 s0[2], s1[2];          // S^T of even / odd tiles
+  bf16x8 p0[2][2], p1[2][2];    // P^T of even / odd tiles
+  float c0 = 1.0f, c1 = 1.0f;   // their O rescale factors
+  bool g0 = false, g1 = false;  // ... and whether any lane's max moved
+
+  // Iteration j: copies of K[j+2] -> K buffer j%2 and V[j] -> V buffer j%2 (both
+  // free: their last readers ran in iteration j-1), S[j+1] from K buffer (j+1)%2,
+  // O += P[j-1] V[j-1] from V buffer (j-1)%2, softmax of S[j].  The flags say
+  // which of the three are present (first, steady, last, drain iterations); in
+  // the steady state the MFMA and softmax work is one straight-line block.
+  enum { kQK = 1, kPV = 2, kSM = 4, kMask = 8 };
+  // Steady-state block, software-ordered: MFMA u (S MFMAs, then PV MFMAs) is
+  // followed by the LDS operand read of MFMA u + kLA and by slice u of the
+  // softmax of the previous tile, and a scheduling barrier closes each slice, so
+  // the VALU work issues while the matrix core runs and only kLA + 1 operands are
+  // in flight.  Softmax slices: 0-3 partial row maxima, 4 the exchange with the
+  // other half-wave and the new running max, 5-20 two exponentials each (packed to
+  // bf16 every 8), 21 the running sum.
+  auto fused = [&](const uint16_t* kt, f32x16 (&sn)[2], const uint16_t* vt,
+                   const bf16x8 (&pp)[2][2], f32x16 (&sc)[2], bf16x8 (&pc)[2][2], float& cc,
+                   bool& gc, uint16_t* kdst, int tk, uint16_t* vdst, int tv)
+      __attribute__((always_inline)) {
+    constexpr int NQ = 2 * (DH / 16), ND = DH / 32, NP = 4 * ND, NM = NQ + NP;
+    constexpr int NS = 22, NU = NM > NS ? NM : NS, kLA = 3;
+    TileMap mk{}, mv{};
+    if constexpr (FAST) {
+      mk = tile_map(tk);
+      mv = tile_map(tv);
+    }
+    const char* kb0 = reinterpret_cast<const char*>(kt);
+    const lds_char* vb0 = (const lds_char*)(vt);
+    bf16x8 op[NM];
+    float pm[4], m_new = 0.0f, rs = 0.0f;
+    float pe[32];
+    auto read = [&](auto uu) __attribute__((always_inline)) {
+      constexpr int u = decltype(uu)::value;
+      if constexpr (u < NQ) {
+        constexpr int t = u / 2, kb = u % 2;
+        op[u] = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(kb0 + (kbase ^ (32u * t)) + kb * 32 * G::ROWB));
+      } else {
+        constexpr int w = u - NQ, kb = w / (2 * ND), s2 = (w / ND) % 2, db = w % ND;
+        const lds_char* p = vb0 + (vbase ^ (64u * db)) + (32 * kb + 16 * s2) * G::ROWB;
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + 8 * G::ROWB));
+        op[u] = __builtin_bit_cast(
+            bf16x8, u32x4{__builtin_bit_cast(u32x2, lo).x, __builtin_bit_cast(u32x2, lo).y,
+                          __builtin_bit_cast(u32x2, hi).x, __builtin_bit_cast(u32x2, hi).y});
+      }
+    };
+    auto mma = [&](auto uu) __attribute__((always_inline)) {
+      constexpr int u = decltype(uu)::value;
+      if constexpr (u < NQ) {
+        constexpr int t = u / 2, kb = u % 2;
+        sn[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            op[u], qreg[t], t == 0 ? f32x16{} : sn[kb], 0, 0, 0);
+      } else {
+        constexpr int w = u - NQ, kb = w / (2 * ND), s2 = (w / ND) % 2, db = w % ND;
+        acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[u], pp[kb][s2], acc_o[db], 0, 0, 0);
+      }
+    };
+    auto smx = [&](auto cc_) __attribute__((always_inline)) {
+      constexpr int c = decltype(cc_)::value;
+      if constexpr (c < 4) {
+        float m = sc[c / 2][8 * (c % 2)];
+#pragma unroll
+        for (int e = 1; e < 8; ++e) m = fmaxf(m, sc[c / 2][8 * (c % 2) + e]);
+        pm[c] = m;
+      } else if constexpr (c == 4) {
+        float mx = fmaxf(fmaxf(pm[0], pm[1]), fmaxf(pm[2], pm[3]));
+        const u32x2 sw = __builtin_bit_cast(
+            u32x2, __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, mx),
+                                                    __builtin_bit_cast(unsigned, mx), false, false));
+        mx = fmaxf(__builtin_bit_cast(float, sw.x), __builtin_bit_cast(float, sw.y));
+        const float m_cand = fmaxf(m_run, mx * a.sl2);
+        const bool up = m_cand > m_run + kMaxSlack;
+        m_new = up ? m_cand : m_run;
+        gc = __ballot(up) != 0ull;
+        cc = __builtin_amdgcn_exp2f(m_run - m_new);
+      } else if constexpr (c < 21) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          constexpr int e = 2 * (c - 5);
+          pe[e + q] = __builtin_amdgcn_exp2f(fmaf(sc[(e + q) / 16][(e + q) % 16], a.sl2, -m_new));
+          rs += pe[e + q];
+        }
+        if constexpr ((2 * (c - 5) + 2) % 8 == 0) {
+          constexpr int g = (2 * (c - 5)) / 8, o = 8 * g;
+          pc[g / 2][g % 2] = __builtin_bit_cast(
+              bf16x8, u32x4{pack_bf16x2(pe[o + 0], pe[o + 1]), pack_bf16x2(pe[o + 2], pe[o + 3]),
+                            pack_bf16x2(pe[o + 4], pe[o + 5]), pack_bf16x2(pe[o + 6], pe[o + 7])});
+          // pinned here: the values are read only in the next iteration, and the
+          // compiler would otherwise sink this work out of the block it overlaps
+          asm volatile("" ::"v"(pc[g / 2][g % 2]));
+        }
+      } else {
+        l_run = l_run * cc + rs;
+        m_run = m_new;
+        asm volatile("" ::"v"(l_run), "v"(cc));
+      }
+    };
+    static_for<0, kLA>([&](auto u) { read(u); });
+    static_for<0, NU>([&](auto uu) {
+      constexpr int u = decltype(uu)::value;
+      if constexpr (FAST && u < G::DPT) copy_fast(IC<0>{}, mk, u, kdst);
+      if constexpr (FAST && u >= G::DPT && u < 2 * G::DPT) copy_fast(IC<1>{}, mv, u - G::DPT, vdst);
+      if constexpr (u + kLA < NM) read(IC<u + kLA>{});
+      if constexpr (u < NM) mma(uu);
+      if constexpr (u < NS) smx(uu);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  };
+  auto step = [&](auto par, auto flags, int j, f32x16 (&sc)[2], f32x16 (&sn)[2],
+                  bf16x8 (&pp)[2][2], bf16x8 (&pc)[2][2], float& cp, bool& gp, float& cc, bool& gc)
+      __attribute__((always_inline)) {
+    constexpr int B = decltype(par)::value, F = decltype(flags)::value;
+    uint16_t* const kmine = B == 0 ? lds_k0 : lds_k1;
+    const uint16_t* const kother = B == 0 ? lds_k1 : lds_k0;
+    uint16_t* const vmine = B == 0 ? lds_v0 : lds_v1;
+    const uint16_t* const vother = B == 0 ? lds_v1 : lds_v0;
+    __builtin_amdgcn_s_waitcnt(0);   // this wave's copies of the previous iteration landed
+    __syncthreads();                 // ... and everyone's; previous readers are done
+    constexpr bool kSteady = F == (kQK | kPV | kSM);
+    if constexpr (!(FAST && kSteady)) {
+      if ((F & kQK) && j + 2 < nt) load_tile(IC<0>{}, j + 2, kmine);
+      if (F & kSM) load_tile(IC<1>{}, j, vmine);
+    }
+    if ((F & kPV) && gp) {
+#pragma unroll
+      for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc_o[db][e] *= cp;
+    }
+    if constexpr (kSteady) {
+      // (FAST: a copy of K past the end re-copies the last tile into a buffer
+      // that is not read again)
+      fused(kother, sn, vother, pp, sc, pc, cc, gc, kmine, min(j + 2, nt - 1), vmine, j);
+    } else {
+      if (F & kQK) qk(kother, sn);
+      if (F & kPV) pv(vother, pp);
+      if (F & kSM) softmax(sc, j, pc, cc, gc, IC<(F & kMask) ? 1 : 0>{});
+    }
+  };
+
+  load_tile(IC<0>{}, 0, lds_k0);
+  if (nt > 1) load_tile(IC<0>{}, 1, lds_k1);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  qk(lds_k0, s0);
+  if (nt == 1) {
+    step(IC<0>{}, IC<kSM | kMask>{}, 0, s0, s1, p1, p0, c1, g1, c0, g0);
+    step(IC<1>{}, IC<kPV>{}, 1, s1, s0, p0, p1, c0, g0, c1, g1);
+  } else {
+    step(IC<0>{}, IC<kQK | kSM>{}, 0, s0, s1, p1, p0, c1, g1, c0, g0);
+    int j = 1;
+    for (; j + 1 <= nt - 2; j += 2) {
+      step(IC<1>{}, IC<kQK | kPV | kSM>{}, j, s1, s0, p0, p1, c0, g0, c1, g1);
+      step(IC<0>{}, IC<kQK | kPV | kSM>{}, j + 1, s0, s1, p1, p0, c1, g1, c0, g0);
+    }
+    if (j <= nt - 2) {
+      step(IC<1>{}, IC<kQK | kPV | kSM>{}, j, s1, s0, p0, p1, c0, g0, c1, g1);
+      ++j;
+    }
+    // j == nt - 1: last softmax (masked), then the drain iteration nt
+    if (j & 1) {
+      step(IC<1>{}, IC<kPV | kSM | kMask>{}, j, s1, s0, p0, p1, c0, g0, c1, g1);
+      step(IC<0>{}, IC<kPV>{}, j + 1, s0, s1, p1, p0, c1, g1, c0, g0);
+    } else {
+      step(IC<0>{}, IC<kPV | kSM | kMask>{}, j, s0, s1, p1, p0, c1, g1, c0, g0);
+      step(IC<1>{}, IC<kPV>{}, j + 1, s1, s0, p0, p1, c0, g0, c1, g1);
+    }
   }
 
   // ---- epilogue: normalise, write O (bf16) and the log-sum-exp
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int qi = qt * BQ + (wave * QB + qb) * 32 + l32;
-    const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
+  {
+    const int qi = qt * 128 + wave * 32 + l32;
+    const float l_tot = l_run + __shfl_xor(l_run, 32);
     const float inv = 1.0f / l_tot;
     if (qi < a.S) {
       uint16_t* op = a.out + (((long long)i * a.S + qi) * a.H + h) * DH + 4 * hf;
@@ -398,21 +535,24 @@ __global__ __launch_bounds__(kThreads, (QB == 1 ? 2 : 1)) void anchor_attn_kerne
       for (int db = 0; db < DH / 32; ++db)
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
-          const u32x2 w = u32x2{pack_bf16x2(acc_o[qb][db][4 * g4 + 0] * inv, acc_o[qb][db][4 * g4 + 1] * inv),
-                                pack_bf16x2(acc_o[qb][db][4 * g4 + 2] * inv, acc_o[qb][db][4 * g4 + 3] * inv)};
+          const u32x2 w = u32x2{pack_bf16x2(acc_o[db][4 * g4 + 0] * inv, acc_o[db][4 * g4 + 1] * inv),
+                                pack_bf16x2(acc_o[db][4 * g4 + 2] * inv, acc_o[db][4 * g4 + 3] * inv)};
           *reinterpret_cast<u32x2*>(op + db * 32 + 8 * g4) = w;
         }
       if (a.lse && hf == 0)
-        a.lse[((long long)i * a.H + h) * a.S + qi] = m_run[qb] * 0.69314718055994531f + logf(l_tot);
+        a.lse[((long long)i * a.H + h) * a.S + qi] = m_run * 0.69314718055994531f + logf(l_tot);
     }
   }
 }
 
-template <int DH, int QB>
+template <int DH>
 cast_status_t launch_dh(AttnArgs a, hipStream_t stream) {
-  a.n_qt = (a.S + 4 * 32 * QB - 1) / (4 * 32 * QB);
+  a.n_qt = (a.S + 127) / 128;
   a.nblocks = a.n_a * a.H * a.n_qt;
-  hipLaunchKernelGGL((anchor_attn_kernel<DH, QB>), dim3(a.nblocks), dim3(kThreads), 0, stream, a);
+  if (a.n0 == 0 && a.Bv >= kBK)
+    hipLaunchKernelGGL((anchor_attn_kernel<DH, true>), dim3(a.nblocks), dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((anchor_attn_kernel<DH, false>), dim3(a.nblocks), dim3(kThreads), 0, stream, a);
   return check_launch("anchor_attn");
 }
 
@@ -445,10 +585,11 @@ cast_status_t launch_anchor_attn(const void* q, const void* k_hist, const void* 
   a.bv_magic = ((1ull << 40) + (unsigned long long)Bv - 1) / (unsigned long long)Bv;
   a.sl2 = scale * 1.4426950408889634f;
   a.hist_bytes = k_eff > 0 ? (long long)M * Bv * H * dh * 2 : 0;
+  a.cur_bytes = n0 > 0 ? (long long)n0 * H * dh * 2 : 0;
   switch (dh) {
-    case 32: return launch_dh<32, 1>(a, stream);
-    case 64: return launch_dh<64, 1>(a, stream);
-    case 128: return launch_dh<128, 1>(a, stream);
+    case 32: return launch_dh<32>(a, stream);
+    case 64: return launch_dh<64>(a, stream);
+    case 128: return launch_dh<128>(a, stream);
     default: return fail(CAST_ERR_UNSUPPORTED, "attn: dh %d", dh);
   }
 }
