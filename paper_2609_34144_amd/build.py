@@ -5,7 +5,8 @@
 Each translation unit is compiled to an object with its own flags, then linked
 into paper_2609_34144_amd/libcast.so.  Packed-fp32 instructions are disabled for
 all device code.  The PAR unit is built with -fno-signed-zeros so that the
-literal zero imaginary parts of real-input tile transforms fold away.
+literal zero imaginary parts of real-input tile transforms fold away; the
+attention unit selects the VGPR form of the MFMA instructions.
 """
 from __future__ import annotations
 
@@ -27,7 +28,9 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
 UNITS = {
     "capi.hip": [],
     "route_kv.hip": [],
-    "anchor_attn.hip": [],
+    # MFMA accumulators in VGPRs: the softmax reads S directly, and the Q operands
+    # are parked in AGPRs by the kernel itself
+    "anchor_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
     "par.hip": ["-fno-signed-zeros"],
 }
 

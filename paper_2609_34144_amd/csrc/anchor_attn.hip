@@ -1,10 +1,10 @@
 // Routed block-sparse anchor attention on gfx950 (Sec. 4.4; App. B.4).
 //
 // Flash-style single pass with bf16 MFMA (v_mfma_f32_32x32x16_bf16) and fp32
-// online softmax.  One workgroup = 4 waves = 128 queries of one (anchor, head);
-// each wave owns 32 queries.  The key sequence of the (anchor, head) is the
-// concatenation [current segment (n0 tokens) ; routed chunk idx[0] ; ... ], walked
-// in tiles of 64 keys.
+// online softmax.  One workgroup = 4 waves = 256 queries of one (anchor, head);
+// each wave owns two blocks of 32 queries.  The key sequence of the (anchor,
+// head) is the concatenation [current segment (n0 tokens) ; routed chunk idx[0] ;
+// ... ], walked in tiles of 64 keys.
 //
 // Data movement: every K and V tile is copied global -> LDS by the buffer unit
 // (buffer_load_dwordx4 ... lds), so no registers or VALU work stage it.  Each
@@ -12,7 +12,7 @@
 // the LDS image be XOR-swizzled against bank conflicts even though the copy
 // writes 1 KB contiguously.  Two K and two V buffers rotate; one barrier per tile.
 //
-// Per wave and tile:
+// Per wave and tile, for each query block:
 //   S^T = K Q^T   A = K rows from LDS (ds_read_b128), B = Q^T held in registers
 //                 for the whole kernel.  The 32x32 accumulator puts one query per
 //                 lane column, so the online-softmax row max / row sum need only
@@ -21,10 +21,12 @@
 //                 bf16; the contraction index order is free, so no data moves),
 //                 A = V^T read from the row-major V tile with the transposing
 //                 LDS load ds_read_b64_tr_b16.
-// Software pipeline: iteration j issues the copies of K[j+2] and V[j], the
-// MFMAs of S[j+1] = K[j+1] Q^T and of O += P[j-1] V[j-1], and the softmax of S[j]
-// (VALU); the three are independent, so the matrix cores and the VALU overlap
-// inside one wave.
+// Each operand read from LDS feeds the MFMAs of both query blocks: with one block
+// per wave the LDS read port, not the matrix core, was the limit.
+// Schedule (per tile j, two straight-line phases of 32 MFMAs each):
+//   phase 1: S[j] for both blocks      || softmax of S[j-1], block 1 (VALU)
+//   phase 2: O += P[j-1] V[j-1], both   || softmax of S[j], block 0
+// so the VALU work of the softmax overlaps the matrix cores inside one wave.
 // Blocks are renumbered so that the Q-tiles of one (anchor, head) land on the
 // same XCD and share its L2 for the routed K/V.
 #include "cast_common.h"
@@ -46,6 +48,7 @@ typedef __attribute__((address_space(3))) char lds_char;
 
 constexpr int kBK = 64;    // keys per tile
 constexpr int kThreads = 256;
+constexpr int kBQ = 256;   // queries per workgroup: 4 waves x 2 blocks of 32
 constexpr int kMaxKeff = kAttnMaxKeff;   // routed chunk indices cached in LDS
 // The running max used for the exponentials moves only when the tile max exceeds
 // it by more than this (log2 units): probabilities stay <= 2^8, harmless in fp32
@@ -88,9 +91,32 @@ __device__ __forceinline__ int xcd_remap(int b, int nb) {
   return (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + j;
 }
 
+// v_max3_f32 (the compiler forms it only from some max chains)
+__device__ __forceinline__ float max3f(float x, float y, float z) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(y), "v"(z));
+  return r;
+}
+
+// Row sums add the bf16 probabilities that enter P V, two per v_dot2 with (1, 1).
+constexpr bf16x2 kOnes2 = {(__bf16)1.0f, (__bf16)1.0f};
+
 // Two floats -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
+}
+
+// Eight probabilities -> one bf16x8 MFMA operand; their bf16 values are added to
+// `rs`.  (The pairs are kept as separate scalars: taking them back out of a
+// 4-word vector for v_dot2 miscompiles with this toolchain.)
+__device__ __forceinline__ bf16x8 pack8_sum(const float* p, float& rs) {
+  const uint32_t w0 = pack_bf16x2(p[0], p[1]), w1 = pack_bf16x2(p[2], p[3]);
+  const uint32_t w2 = pack_bf16x2(p[4], p[5]), w3 = pack_bf16x2(p[6], p[7]);
+  rs = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w0), kOnes2, rs, false);
+  rs = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w1), kOnes2, rs, false);
+  rs = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w2), kOnes2, rs, false);
+  rs = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w3), kOnes2, rs, false);
+  return __builtin_bit_cast(bf16x8, u32x4{w0, w1, w2, w3});
 }
 
 constexpr int kBufDword3 = 0x00020000;   // 32-bit data format, gfx9-family V#
@@ -122,9 +148,15 @@ __device__ __forceinline__ constexpr int vswz(int r, int cpr) {
 
 // FAST: no current segment and chunks of >= 64 rows, so every tile takes the
 // uniform two-chunk mapping and its copies can be issued inside the MFMA block.
+// Each wave owns QB = 2 blocks of 32 queries: every K / V operand read from LDS
+// feeds two MFMAs, which halves the LDS read traffic per MFMA (with one block
+// per wave the LDS port, not the matrix core, is the limit).  The O accumulators
+// live in the AGPR file; one workgroup runs per CU.
 template <int DH, bool FAST>
-__global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
+  constexpr int QB = 2;
   using G = Geo<DH>;
+  constexpr int BQ = kBQ;
   // separate objects, so the compiler can tell the copy targets from the buffers
   // being read and does not wait for in-flight copies before unrelated LDS reads
   __shared__ __attribute__((aligned(1024))) uint16_t lds_k0[kBK * DH];
@@ -151,17 +183,27 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
     sidx[tid] = 0;
   }
 
-  // ---- Q^T operand in registers: the lane holds query qt*128 + wave*32 + l32,
-  //      d = 16t + 8hf .. +8
-  bf16x8 qreg[DH / 16];
-  {
-    const int qi = qt * 128 + wave * 32 + l32;
+  // ---- Q^T operands in registers: for query block qb the lane holds query
+  //      qt*BQ + (wave*QB + qb)*32 + l32, d = 16t + 8hf .. +8
+  bf16x8 qreg[QB][DH / 16];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int qi = qt * BQ + (wave * QB + qb) * 32 + l32;
     // rows past S load the last query; their outputs are never stored
     const int qc = qi < a.S ? qi : a.S - 1;
     const uint16_t* qp = a.q + (((long long)i * a.S + qc) * a.H + h) * DH + 8 * hf;
 #pragma unroll
-    for (int t = 0; t < DH / 16; ++t)
-      qreg[t] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qp + 16 * t));
+    for (int t = 0; t < DH / 16; ++t) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(qp + 16 * t);
+      // parked in the AGPR file (the MFMAs read their B operand there), which
+      // leaves the VGPRs to S, P and the softmax
+      unsigned x0, x1, x2, x3;
+      asm volatile("v_accvgpr_write_b32 %0, %1" : "=a"(x0) : "v"(v.x));
+      asm volatile("v_accvgpr_write_b32 %0, %1" : "=a"(x1) : "v"(v.y));
+      asm volatile("v_accvgpr_write_b32 %0, %1" : "=a"(x2) : "v"(v.z));
+      asm volatile("v_accvgpr_write_b32 %0, %1" : "=a"(x3) : "v"(v.w));
+      qreg[qb][t] = __builtin_bit_cast(bf16x8, u32x4{x0, x1, x2, x3});
+    }
   }
   __syncthreads();   // sidx visible to every wave
 
@@ -180,19 +222,18 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
   auto copy16 = [&](__amdgpu_buffer_rsrc_t rs, uint16_t* dst, int n, unsigned off)
       __attribute__((always_inline)) {
     // recomputed at each use (the laundering stops the compiler from keeping the
-    // 16 LDS bases of all buffers live in scalar registers across the loop)
+    // LDS bases of all buffers live in scalar registers across the loop)
     int wbase = wave * G::DPT * 1024;
     asm volatile("" : "+s"(wbase));
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
         rs, (lds_void*)(reinterpret_cast<char*>(dst) + wbase + n * 1024), 16, (int)off, 0, 0, 0);
   };
-  // Copy tile `tile` of K (IsV = 0) or V (IsV = 1) into `dst`.  Row j of the tile is
-  // sequence row r = 64*tile + j: current segment rows r < n0, then routed chunk
-  // rows.  History-only tiles with chunks of >= 64 rows meet at most two routed
-  // slots s0, s0 + 1, whose rows are contiguous, so row j sits at
-  // (j < split ? base0 : base1) + j * row_bytes with wave-uniform base0, base1,
-  // split.  Rows past the end read real rows (clamped, or of the padded slot);
-  // their logits are masked to -inf and add nothing.
+  // Row j of tile `tile` is sequence row r = 64*tile + j: current segment rows
+  // r < n0, then routed chunk rows.  History-only tiles with chunks of >= 64 rows
+  // meet at most two routed slots s0, s0 + 1, whose rows are contiguous, so row j
+  // sits at (j < split ? base0 : base1) + j * row_bytes with wave-uniform base0,
+  // base1, split.  Rows past the end read real rows (clamped, or of the padded
+  // slot); their logits are masked to -inf and add nothing.
   struct TileMap { unsigned base0, base1; int split; };
   auto tile_map = [&](int tile) __attribute__((always_inline)) -> TileMap {
     const int u0 = tile * kBK - a.n0;                     // first chunk-part row of the tile
@@ -211,9 +252,9 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
     const unsigned off = (r < m.split ? m.base0 : m.base1) + (unsigned)r * row_bytes + slot_off(n, IsV);
     copy16(tensor_rsrc(IsV ? a.v : a.k, a.hist_bytes), dst, n, off);
   };
+  // Copy tile `tile` of K (is_v = 0) or V (is_v = 1) into `dst`.
   auto load_tile = [&](auto is_v, int tile, uint16_t* dst) __attribute__((always_inline)) {
     constexpr bool IsV = decltype(is_v)::value != 0;
-    const __amdgpu_buffer_rsrc_t rh = tensor_rsrc(IsV ? a.v : a.k, a.hist_bytes);
     if (FAST || (tile * kBK >= a.n0 && a.Bv >= kBK)) {
       const TileMap m = tile_map(tile);
 #pragma unroll
@@ -221,6 +262,7 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
     } else {
       // tiles that touch the current segment, or chunks shorter than a tile:
       // per-row slot by multiply-shift
+      const __amdgpu_buffer_rsrc_t rh = tensor_rsrc(IsV ? a.v : a.k, a.hist_bytes);
 #pragma unroll
       for (int n = 0; n < G::DPT; ++n) {
         int r = tile * kBK + slot_row(n);
@@ -257,277 +299,236 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
     const int c = 2 * (gq & 1) + ((la & 3) >> 1);
     vbase = (unsigned)(vr * G::ROWB + ((c ^ vswz(vr, G::CPR)) * 16) + 8 * (la & 1));
   }
-
-  f32x16 acc_o[DH / 32];
-#pragma unroll
-  for (int db = 0; db < DH / 32; ++db)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) acc_o[db][e] = 0.0f;
-  float m_run = -INFINITY, l_run = 0.0f;
-
-  // S^T = K Q^T for the 64 keys of the tile in `kt`
-  auto qk = [&](const uint16_t* kt, f32x16 (&acc)[2]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[kb][e] = 0.0f;
-    const char* kb0 = reinterpret_cast<const char*>(kt);
-#pragma unroll
-    for (int t = 0; t < DH / 16; ++t)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const bf16x8 ka = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(kb0 + (kbase ^ (32u * t)) + kb * 32 * G::ROWB));
-        acc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qreg[t], acc[kb], 0, 0, 0);
-      }
+  // operand reads: K rows (block kb, d-chunk t) and V^T (d-block db, keys of (kb, s))
+  auto read_k = [&](const uint16_t* kt, int t, int kb) __attribute__((always_inline)) -> bf16x8 {
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
+        reinterpret_cast<const char*>(kt) + (kbase ^ (32u * t)) + kb * 32 * G::ROWB));
   };
-  // O^T += V^T P^T for the tile in `vt`.  MFMA (kb, s) contracts the keys
-  // 32kb + 16s + 4hf + {0..3} and 32kb + 16s + 8 + 4hf + {0..3}: the S^T accumulator
-  // rows that lane holds as p[8s .. 8s+7] of block kb.
-  auto pv = [&](const uint16_t* vt, const bf16x8 (&pb)[2][2]) __attribute__((always_inline)) {
-    const lds_char* vb0 = (const lds_char*)(vt);
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int s = 0; s < 2; ++s)
-#pragma unroll
-        for (int db = 0; db < DH / 32; ++db) {
-          const lds_char* p = vb0 + (vbase ^ (64u * db)) + (32 * kb + 16 * s) * G::ROWB;
-          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
-          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + 8 * G::ROWB));
-          const bf16x8 va = __builtin_bit_cast(
-              bf16x8, u32x4{__builtin_bit_cast(u32x2, lo).x, __builtin_bit_cast(u32x2, lo).y,
-                            __builtin_bit_cast(u32x2, hi).x, __builtin_bit_cast(u32x2, hi).y});
-          acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kb][s], acc_o[db], 0, 0, 0);
-        }
+  auto read_v = [&](const uint16_t* vt, int db, int kb, int s2) __attribute__((always_inline)) -> bf16x8 {
+    const lds_char* p = (const lds_char*)(vt) + (vbase ^ (64u * db)) + (32 * kb + 16 * s2) * G::ROWB;
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + 8 * G::ROWB));
+    return __builtin_bit_cast(bf16x8, u32x4{__builtin_bit_cast(u32x2, lo).x, __builtin_bit_cast(u32x2, lo).y,
+                                            __builtin_bit_cast(u32x2, hi).x, __builtin_bit_cast(u32x2, hi).y});
   };
-  // online softmax of tile `tile` (log2 domain), one query per lane column
-  auto softmax = [&](f32x16 (&acc)[2], int tile, bf16x8 (&pb)[2][2], float& corr, bool& grew,
-                     auto mask) __attribute__((always_inline)) {
+
+  f32x16 acc_o[QB][DH / 32];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc_o[qb][db][e] = 0.0f;
+  float m_run[QB], l_run[QB];
+#pragma unroll
+  // (a finite floor, so that an all -inf tile leaves m_run, l_run unchanged)
+  for (int qb = 0; qb < QB; ++qb) { m_run[qb] = -1e30f; l_run[qb] = 0.0f; }
+
+  // new running max of block qb from this tile's row max `mx` (one exchange with
+  // the other half-wave); the max used for the exponentials moves only by more
+  // than kMaxSlack.  Returns whether it moved.
+  auto new_max = [&](float mx, int qb, float& m_new, float& corr) __attribute__((always_inline)) -> bool {
+    const u32x2 sw = __builtin_bit_cast(
+        u32x2, __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, mx),
+                                                __builtin_bit_cast(unsigned, mx), false, false));
+    mx = fmaxf(__builtin_bit_cast(float, sw.x), __builtin_bit_cast(float, sw.y));
+    const float m_cand = fmaxf(m_run[qb], mx * a.sl2);
+    const bool up = m_cand > m_run[qb] + kMaxSlack;
+    m_new = up ? m_cand : m_run[qb];
+    corr = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
+    return up;
+  };
+
+  using SBlk = f32x16[2];      // S^T of one 32-query block and 64 keys
+  using PBlk = bf16x8[2][2];   // its P^T operands
+  // keys past the end of the sequence get logit -inf (the last tile, and the
+  // throw-away tile nt)
+  auto mask_tile = [&](SBlk& ss, int tile) __attribute__((always_inline)) {
     const int key0 = tile * kBK;
-    if (decltype(mask)::value) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = key0 + kb * 32 + 8 * (e / 4) + 4 * hf + (e % 4);
-          if (key >= a.L) acc[kb][e] = -INFINITY;
-        }
-    }
-    float mx = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, acc[kb][e]);
-    {
-      const u32x2 sw = __builtin_bit_cast(
-          u32x2, __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, mx),
-                                                  __builtin_bit_cast(unsigned, mx), false, false));
-      mx = fmaxf(__builtin_bit_cast(float, sw.x), __builtin_bit_cast(float, sw.y));
-    }
-    const float m_cand = fmaxf(m_run, mx * a.sl2);
-    const bool up = m_cand > m_run + kMaxSlack;
-    const float m_new = up ? m_cand : m_run;
-    grew = __ballot(up) != 0ull;
-    corr = __builtin_amdgcn_exp2f(m_run - m_new);
-    float rs = 0.0f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      float p[16];
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        p[e] = __builtin_amdgcn_exp2f(fmaf(acc[kb][e], a.sl2, -m_new));
-        rs += p[e];
+        const int key = key0 + kb * 32 + 8 * (e / 4) + 4 * hf + (e % 4);
+        if (key >= a.L) ss[kb][e] = -INFINITY;
       }
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        const u32x4 w = u32x4{pack_bf16x2(p[8 * s + 0], p[8 * s + 1]), pack_bf16x2(p[8 * s + 2], p[8 * s + 3]),
-                              pack_bf16x2(p[8 * s + 4], p[8 * s + 5]), pack_bf16x2(p[8 * s + 6], p[8 * s + 7])};
-        pb[kb][s] = __builtin_bit_cast(bf16x8, w);
-      }
-    }
-    l_run = l_run * corr + rs;
-    m_run = m_new;
   };
+  using SAcc = SBlk[QB];
+  using PAcc = PBlk[QB];
+  constexpr int ND = DH / 32, NR = 2 * (DH / 16);   // operand reads per phase (K: 2 per t, V: 4 per db)
+  constexpr int NM = QB * NR;                       // MFMAs per phase
 
-  const int nt = (a.L + kBK - 1) / kBK;
-  f32x16 s0[2], s1[2];          // S^T of even / odd tiles
-  bf16x8 p0[2][2], p1[2][2];    // P^T of even / odd tiles
-  float c0 = 1.0f, c1 = 1.0f;   // their O rescale factors
-  bool g0 = false, g1 = false;  // ... and whether any lane's max moved
-
-  // Iteration j: copies of K[j+2] -> K buffer j%2 and V[j] -> V buffer j%2 (both
-  // free: their last readers ran in iteration j-1), S[j+1] from K buffer (j+1)%2,
-  // O += P[j-1] V[j-1] from V buffer (j-1)%2, softmax of S[j].  The flags say
-  // which of the three are present (first, steady, last, drain iterations); in
-  // the steady state the MFMA and softmax work is one straight-line block.
-  enum { kQK = 1, kPV = 2, kSM = 4, kMask = 8 };
-  // Steady-state block, software-ordered: MFMA u (S MFMAs, then PV MFMAs) is
-  // followed by the LDS operand read of MFMA u + kLA and by slice u of the
-  // softmax of the previous tile, and a scheduling barrier closes each slice, so
-  // the VALU work issues while the matrix core runs and only kLA + 1 operands are
-  // in flight.  Softmax slices: 0-3 partial row maxima, 4 the exchange with the
-  // other half-wave and the new running max, 5-20 two exponentials each (packed to
-  // bf16 every 8), 21 the running sum.
-  auto fused = [&](const uint16_t* kt, f32x16 (&sn)[2], const uint16_t* vt,
-                   const bf16x8 (&pp)[2][2], f32x16 (&sc)[2], bf16x8 (&pc)[2][2], float& cc,
-                   bool& gc, uint16_t* kdst, int tk, uint16_t* vdst, int tv)
-      __attribute__((always_inline)) {
-    constexpr int NQ = 2 * (DH / 16), ND = DH / 32, NP = 4 * ND, NM = NQ + NP;
-    constexpr int NS = 22, NU = NM > NS ? NM : NS, kLA = 3;
+  // ---- one phase = NM MFMAs sharing NR operand reads (each read feeds the QB
+  //      query blocks), interleaved slice by slice with the softmax of one
+  //      32-query block and, optionally, the tile copies.  A scheduling barrier
+  //      closes each slice, so the VALU work issues while the matrix core runs.
+  //      Softmax slices: 0-3 running max (v_max3 chain), 4 exchange with the other
+  //      half-wave and new max, 5.. the 32 exponentials (packed to bf16 and summed
+  //      every 8).
+  //   IsPV = 0: S^T[qb] = K Q^T[qb] from the K tile `src` into `sn`.
+  //   IsPV = 1: O^T[qb] += V^T P^T[qb] from the V tile `src` with operands `pp`.
+  auto phase = [&](auto is_pv, auto do_mm, auto do_sm, auto do_copy, const uint16_t* src, SAcc& sn,
+                   const PAcc& pp, SBlk& ss, PBlk& ps, float& corr, bool& up, int qbs, uint16_t* kdst,
+                   int tk, uint16_t* vdst, int tv) __attribute__((always_inline)) {
+    constexpr bool IsPV = decltype(is_pv)::value != 0, MM = decltype(do_mm)::value != 0;
+    constexpr bool SM = decltype(do_sm)::value != 0;
+    constexpr bool COPY = decltype(do_copy)::value != 0;
+    constexpr int NSL = (MM ? NM : 0) > 32 ? NM : 32;
+    constexpr int kLA = 2;
     TileMap mk{}, mv{};
-    if constexpr (FAST) {
+    if constexpr (COPY) {
       mk = tile_map(tk);
       mv = tile_map(tv);
     }
-    const char* kb0 = reinterpret_cast<const char*>(kt);
-    const lds_char* vb0 = (const lds_char*)(vt);
-    bf16x8 op[NM];
-    float pm[4], m_new = 0.0f, rs = 0.0f;
+    bf16x8 op[NR];
+    float pm = 0.0f, m_new = 0.0f, rs = 0.0f;
     float pe[32];
-    auto read = [&](auto uu) __attribute__((always_inline)) {
-      constexpr int u = decltype(uu)::value;
-      if constexpr (u < NQ) {
-        constexpr int t = u / 2, kb = u % 2;
-        op[u] = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const u32x4*>(kb0 + (kbase ^ (32u * t)) + kb * 32 * G::ROWB));
-      } else {
-        constexpr int w = u - NQ, kb = w / (2 * ND), s2 = (w / ND) % 2, db = w % ND;
-        const lds_char* p = vb0 + (vbase ^ (64u * db)) + (32 * kb + 16 * s2) * G::ROWB;
-        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
-        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + 8 * G::ROWB));
-        op[u] = __builtin_bit_cast(
-            bf16x8, u32x4{__builtin_bit_cast(u32x2, lo).x, __builtin_bit_cast(u32x2, lo).y,
-                          __builtin_bit_cast(u32x2, hi).x, __builtin_bit_cast(u32x2, hi).y});
-      }
+    auto read = [&](auto rr) __attribute__((always_inline)) {
+      constexpr int r = decltype(rr)::value;
+      if constexpr (!IsPV) op[r] = read_k(src, r / 2, r % 2);
+      else op[r] = read_v(src, r % ND, r / (2 * ND), (r / ND) % 2);
     };
     auto mma = [&](auto uu) __attribute__((always_inline)) {
-      constexpr int u = decltype(uu)::value;
-      if constexpr (u < NQ) {
-        constexpr int t = u / 2, kb = u % 2;
-        sn[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            op[u], qreg[t], t == 0 ? f32x16{} : sn[kb], 0, 0, 0);
+      constexpr int u = decltype(uu)::value, r = u / QB, qb = u % QB;
+      if constexpr (!IsPV) {
+        constexpr int t = r / 2, kb = r % 2;
+        sn[qb][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[r], qreg[qb][t], t == 0 ? f32x16{} : sn[qb][kb],
+                                                             0, 0, 0);
       } else {
-        constexpr int w = u - NQ, kb = w / (2 * ND), s2 = (w / ND) % 2, db = w % ND;
-        acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[u], pp[kb][s2], acc_o[db], 0, 0, 0);
+        constexpr int kb = r / (2 * ND), s2 = (r / ND) % 2, db = r % ND;
+        acc_o[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op[r], pp[qb][kb][s2], acc_o[qb][db], 0, 0, 0);
       }
     };
+    // first exponential of slice c >= 5: the 32 spread evenly over slices 5 .. NSL-1
+    auto e_first = [](int c) constexpr { return c <= 5 ? 0 : ((c - 5) * 32) / (NSL - 5); };
     auto smx = [&](auto cc_) __attribute__((always_inline)) {
       constexpr int c = decltype(cc_)::value;
       if constexpr (c < 4) {
-        float m = sc[c / 2][8 * (c % 2)];
-#pragma unroll
-        for (int e = 1; e < 8; ++e) m = fmaxf(m, sc[c / 2][8 * (c % 2) + e]);
-        pm[c] = m;
+        static_for<4 * c, 4 * c + 4>([&](auto kk) {
+          constexpr int k = decltype(kk)::value;
+          if constexpr (k == 0) {
+            pm = max3f(ss[0][0], ss[0][1], ss[0][2]);
+          } else if constexpr (k < 15) {
+            constexpr int v = 2 * k + 1;
+            pm = max3f(pm, ss[v / 16][v % 16], ss[(v + 1) / 16][(v + 1) % 16]);
+          } else {
+            pm = fmaxf(pm, ss[1][15]);
+          }
+        });
       } else if constexpr (c == 4) {
-        float mx = fmaxf(fmaxf(pm[0], pm[1]), fmaxf(pm[2], pm[3]));
-        const u32x2 sw = __builtin_bit_cast(
-            u32x2, __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, mx),
-                                                    __builtin_bit_cast(unsigned, mx), false, false));
-        mx = fmaxf(__builtin_bit_cast(float, sw.x), __builtin_bit_cast(float, sw.y));
-        const float m_cand = fmaxf(m_run, mx * a.sl2);
-        const bool up = m_cand > m_run + kMaxSlack;
-        m_new = up ? m_cand : m_run;
-        gc = __ballot(up) != 0ull;
-        cc = __builtin_amdgcn_exp2f(m_run - m_new);
-      } else if constexpr (c < 21) {
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          constexpr int e = 2 * (c - 5);
-          pe[e + q] = __builtin_amdgcn_exp2f(fmaf(sc[(e + q) / 16][(e + q) % 16], a.sl2, -m_new));
-          rs += pe[e + q];
-        }
-        if constexpr ((2 * (c - 5) + 2) % 8 == 0) {
-          constexpr int g = (2 * (c - 5)) / 8, o = 8 * g;
-          pc[g / 2][g % 2] = __builtin_bit_cast(
-              bf16x8, u32x4{pack_bf16x2(pe[o + 0], pe[o + 1]), pack_bf16x2(pe[o + 2], pe[o + 3]),
-                            pack_bf16x2(pe[o + 4], pe[o + 5]), pack_bf16x2(pe[o + 6], pe[o + 7])});
-          // pinned here: the values are read only in the next iteration, and the
-          // compiler would otherwise sink this work out of the block it overlaps
-          asm volatile("" ::"v"(pc[g / 2][g % 2]));
-        }
+        up = new_max(pm, qbs, m_new, corr);
       } else {
-        l_run = l_run * cc + rs;
-        m_run = m_new;
-        asm volatile("" ::"v"(l_run), "v"(cc));
+        constexpr int e0 = e_first(c), e1 = e_first(c + 1);
+        static_for<e0, e1>([&](auto ee) {
+          constexpr int e = decltype(ee)::value;
+          pe[e] = __builtin_amdgcn_exp2f(fmaf(ss[e / 16][e % 16], a.sl2, -m_new));
+          if constexpr (e % 8 == 7) {
+            constexpr int g = e / 8;
+            ps[g / 2][g % 2] = pack8_sum(&pe[8 * g], rs);
+            // pinned here: the values are read only later, and the compiler would
+            // otherwise sink this work out of the block it overlaps
+            asm volatile("" ::"v"(ps[g / 2][g % 2]));
+          }
+          if constexpr (e == 31) {
+            l_run[qbs] = l_run[qbs] * corr + rs;
+            m_run[qbs] = m_new;
+            asm volatile("" ::"v"(l_run[qbs]), "v"(corr));
+          }
+        });
       }
     };
-    static_for<0, kLA>([&](auto u) { read(u); });
-    static_for<0, NU>([&](auto uu) {
+    if constexpr (MM) static_for<0, kLA>([&](auto r) { read(r); });
+    static_for<0, NSL>([&](auto uu) {
       constexpr int u = decltype(uu)::value;
-      if constexpr (FAST && u < G::DPT) copy_fast(IC<0>{}, mk, u, kdst);
-      if constexpr (FAST && u >= G::DPT && u < 2 * G::DPT) copy_fast(IC<1>{}, mv, u - G::DPT, vdst);
-      if constexpr (u + kLA < NM) read(IC<u + kLA>{});
-      if constexpr (u < NM) mma(uu);
-      if constexpr (u < NS) smx(uu);
+      if constexpr (COPY && u < G::DPT) copy_fast(IC<0>{}, mk, u, kdst);
+      if constexpr (COPY && u >= G::DPT && u < 2 * G::DPT) copy_fast(IC<1>{}, mv, u - G::DPT, vdst);
+      if constexpr (MM) {
+        // the read for operand r + kLA is issued with the first MFMA of operand r
+        if constexpr (u % QB == 0 && u / QB + kLA < NR) read(IC<u / QB + kLA>{});
+        if constexpr (u < NM) mma(uu);
+      }
+      if constexpr (SM) smx(uu);
       __builtin_amdgcn_sched_barrier(0);
     });
   };
-  auto step = [&](auto par, auto flags, int j, f32x16 (&sc)[2], f32x16 (&sn)[2],
-                  bf16x8 (&pp)[2][2], bf16x8 (&pc)[2][2], float& cp, bool& gp, float& cc, bool& gc)
-      __attribute__((always_inline)) {
-    constexpr int B = decltype(par)::value, F = decltype(flags)::value;
-    uint16_t* const kmine = B == 0 ? lds_k0 : lds_k1;
-    const uint16_t* const kother = B == 0 ? lds_k1 : lds_k0;
-    uint16_t* const vmine = B == 0 ? lds_v0 : lds_v1;
-    const uint16_t* const vother = B == 0 ? lds_v1 : lds_v0;
-    __builtin_amdgcn_s_waitcnt(0);   // this wave's copies of the previous iteration landed
-    __syncthreads();                 // ... and everyone's; previous readers are done
-    constexpr bool kSteady = F == (kQK | kPV | kSM);
-    if constexpr (!(FAST && kSteady)) {
-      if ((F & kQK) && j + 2 < nt) load_tile(IC<0>{}, j + 2, kmine);
-      if (F & kSM) load_tile(IC<1>{}, j, vmine);
-    }
-    if ((F & kPV) && gp) {
-#pragma unroll
-      for (int db = 0; db < DH / 32; ++db)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) acc_o[db][e] *= cp;
-    }
-    if constexpr (kSteady) {
-      // (FAST: a copy of K past the end re-copies the last tile into a buffer
-      // that is not read again)
-      fused(kother, sn, vother, pp, sc, pc, cc, gc, kmine, min(j + 2, nt - 1), vmine, j);
-    } else {
-      if (F & kQK) qk(kother, sn);
-      if (F & kPV) pv(vother, pp);
-      if (F & kSM) softmax(sc, j, pc, cc, gc, IC<(F & kMask) ? 1 : 0>{});
-    }
-  };
 
-  load_tile(IC<0>{}, 0, lds_k0);
-  if (nt > 1) load_tile(IC<0>{}, 1, lds_k1);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  qk(lds_k0, s0);
-  if (nt == 1) {
-    step(IC<0>{}, IC<kSM | kMask>{}, 0, s0, s1, p1, p0, c1, g1, c0, g0);
-    step(IC<1>{}, IC<kPV>{}, 1, s1, s0, p0, p1, c0, g0, c1, g1);
-  } else {
-    step(IC<0>{}, IC<kQK | kSM>{}, 0, s0, s1, p1, p0, c1, g1, c0, g0);
-    int j = 1;
-    for (; j + 1 <= nt - 2; j += 2) {
-      step(IC<1>{}, IC<kQK | kPV | kSM>{}, j, s1, s0, p0, p1, c0, g0, c1, g1);
-      step(IC<0>{}, IC<kQK | kPV | kSM>{}, j + 1, s0, s1, p1, p0, c1, g1, c0, g0);
-    }
-    if (j <= nt - 2) {
-      step(IC<1>{}, IC<kQK | kPV | kSM>{}, j, s1, s0, p0, p1, c0, g0, c1, g1);
-      ++j;
-    }
-    // j == nt - 1: last softmax (masked), then the drain iteration nt
-    if (j & 1) {
-      step(IC<1>{}, IC<kPV | kSM | kMask>{}, j, s1, s0, p0, p1, c0, g0, c1, g1);
-      step(IC<0>{}, IC<kPV>{}, j + 1, s0, s1, p1, p0, c1, g1, c0, g0);
-    } else {
-      step(IC<0>{}, IC<kPV | kSM | kMask>{}, j, s0, s1, p1, p0, c1, g1, c0, g0);
-      step(IC<1>{}, IC<kPV>{}, j + 1, s1, s0, p0, p1, c0, g0, c1, g1);
-    }
+  const int nt = (a.L + kBK - 1) / kBK;
+  SAcc sA, sB;        // S^T of even / odd tiles
+  PAcc pA, pB;        // P^T of even / odd tiles
+  float c0A = 1.0f, c1A = 1.0f, c0B = 1.0f, c1B = 1.0f;   // O rescale factors, by block and tile parity
+  bool u0A = false, u1A = false, u0B = false, u1B = false;
+  // tile -1 (odd): logits -inf and probabilities 0, so the first iteration's
+  // softmax of its block 1 and its P V add nothing
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) sB[1][kb][e] = -INFINITY;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) pB[qb][kb][s2] = bf16x8{};
   }
 
-  // ---- epilogue: normalise, write O (bf16) and the log-sum-exp
+  // Iteration j = 0 .. nt (tiles: K[j] in K buffer j%2, V[j-1] in V buffer (j-1)%2):
+  //   copies K[j+1] -> K buffer (j+1)%2 and V[j] -> V buffer j%2 (their last
+  //   readers ran in iteration j-1; past the end the last tile is copied again
+  //   into a buffer that is not read for real data);
+  //   phase 1: S[j] = K[j] Q^T (both blocks)     || softmax of S[j-1], block 1
+  //   O rescale (both blocks by tile j-1's factors)
+  //   phase 2: O += P[j-1] V[j-1] (both blocks)    || softmax of S[j], block 0
+  // Iteration 0 meets tile -1 (all -inf, P = 0, V buffer zeroed); iteration nt
+  // computes a throw-away S from a stale K tile whose block-0 softmax is fully
+  // masked.  Every iteration runs the same straight-line phases.
+  auto step = [&](auto par, int j, SAcc& sc, SAcc& sp, PAcc& pc, PAcc& pp, float& c0c, bool& u0c,
+                  float& c0p, bool& u0p, float& c1p, bool& u1p) __attribute__((always_inline)) {
+    constexpr int B = decltype(par)::value;
+    const uint16_t* const kcur = B == 0 ? lds_k0 : lds_k1;   // K[j]
+    uint16_t* const knext = B == 0 ? lds_k1 : lds_k0;        // K[j+1]
+    uint16_t* const vcur = B == 0 ? lds_v0 : lds_v1;         // V[j]
+    const uint16_t* const vprev = B == 0 ? lds_v1 : lds_v0;  // V[j-1]
+    const int tk = min(j + 1, nt - 1), tv = min(j, nt - 1);
+    __builtin_amdgcn_s_waitcnt(0);   // this wave's copies of the previous iteration landed
+    __syncthreads();                 // ... and everyone's; previous readers are done
+    if constexpr (!FAST) {
+      load_tile(IC<0>{}, tk, knext);
+      load_tile(IC<1>{}, tv, vcur);
+    }
+    if (j == nt) mask_tile(sp[1], j - 1);
+    phase(IC<0>{}, IC<1>{}, IC<1>{}, IC<FAST ? 1 : 0>{}, kcur, sc, pp, sp[1], pp[1], c1p, u1p, 1,
+          knext, tk, vcur, tv);
+    // O rescale before O += P[j-1] V[j-1]: block 0 by tile j-1's factor (phase 2 of
+    // the previous iteration), block 1 by the one just computed
+    if (__ballot(u0p || u1p) != 0ull) {
+      // one accumulator at a time (they live in AGPRs; this bounds the VGPR copies)
+      static_for<0, QB * ND>([&](auto kk) {
+        constexpr int qb = decltype(kk)::value / ND, db = decltype(kk)::value % ND;
+        acc_o[qb][db] *= (qb == 0 ? c0p : c1p);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    }
+    if (j >= nt - 1) mask_tile(sc[0], j);
+    phase(IC<1>{}, IC<1>{}, IC<1>{}, IC<0>{}, vprev, sc, pp, sc[0], pc[0], c0c, u0c, 0, nullptr, 0,
+          nullptr, 0);
+  };
+
+  // zero the V buffer that iteration 0 reads as V[-1] (P[-1] = 0 must not meet NaN)
   {
-    const int qi = qt * 128 + wave * 32 + l32;
-    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    u32x4* z = reinterpret_cast<u32x4*>(lds_v1);
+    for (int x = tid; x < kBK * DH / 8; x += kThreads) z[x] = u32x4{0u, 0u, 0u, 0u};
+  }
+  load_tile(IC<0>{}, 0, lds_k0);
+  int j = 0;
+  for (; j + 1 <= nt; j += 2) {
+    step(IC<0>{}, j, sA, sB, pA, pB, c0A, u0A, c0B, u0B, c1B, u1B);
+    step(IC<1>{}, j + 1, sB, sA, pB, pA, c0B, u0B, c0A, u0A, c1A, u1A);
+  }
+  if (j <= nt) step(IC<0>{}, j, sA, sB, pA, pB, c0A, u0A, c0B, u0B, c1B, u1B);
+
+  // ---- epilogue: normalise, write O (bf16) and the log-sum-exp
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int qi = qt * BQ + (wave * QB + qb) * 32 + l32;
+    const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
     const float inv = 1.0f / l_tot;
     if (qi < a.S) {
       uint16_t* op = a.out + (((long long)i * a.S + qi) * a.H + h) * DH + 4 * hf;
@@ -535,19 +536,19 @@ __global__ __launch_bounds__(kThreads, 2) void anchor_attn_kernel(AttnArgs a) {
       for (int db = 0; db < DH / 32; ++db)
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
-          const u32x2 w = u32x2{pack_bf16x2(acc_o[db][4 * g4 + 0] * inv, acc_o[db][4 * g4 + 1] * inv),
-                                pack_bf16x2(acc_o[db][4 * g4 + 2] * inv, acc_o[db][4 * g4 + 3] * inv)};
+          const u32x2 w = u32x2{pack_bf16x2(acc_o[qb][db][4 * g4 + 0] * inv, acc_o[qb][db][4 * g4 + 1] * inv),
+                                pack_bf16x2(acc_o[qb][db][4 * g4 + 2] * inv, acc_o[qb][db][4 * g4 + 3] * inv)};
           *reinterpret_cast<u32x2*>(op + db * 32 + 8 * g4) = w;
         }
       if (a.lse && hf == 0)
-        a.lse[((long long)i * a.H + h) * a.S + qi] = m_run * 0.69314718055994531f + logf(l_tot);
+        a.lse[((long long)i * a.H + h) * a.S + qi] = m_run[qb] * 0.69314718055994531f + logf(l_tot);
     }
   }
 }
 
 template <int DH>
 cast_status_t launch_dh(AttnArgs a, hipStream_t stream) {
-  a.n_qt = (a.S + 127) / 128;
+  a.n_qt = (a.S + kBQ - 1) / kBQ;
   a.nblocks = a.n_a * a.H * a.n_qt;
   if (a.n0 == 0 && a.Bv >= kBK)
     hipLaunchKernelGGL((anchor_attn_kernel<DH, true>), dim3(a.nblocks), dim3(kThreads), 0, stream, a);
