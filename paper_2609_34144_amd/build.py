@@ -25,14 +25,21 @@ ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-Wall", "-Wno-unused-function", "-Wno-unused-variable"]
-UNITS = {
-    "capi.hip": [],
-    "route_kv.hip": [],
+# (source, object name, extra flags); par_fused.hip is compiled once per
+# bottom-remainder height of the 8x8 tiling (one row of the fused-kernel table)
+# (source, object name, extra flags), longest first; par_fused.hip is compiled
+# once per bottom-remainder height of the 8x8 tiling (one row of the
+# fused-kernel table)
+UNITS = [("par.hip", "par", ["-fno-signed-zeros"])] + [
+    ("par_fused.hip", f"par_fused_{hr}", ["-fno-signed-zeros", f"-DCAST_PAR_HR={hr}"])
+    for hr in range(8, 0, -1)
+] + [
     # MFMA accumulators in VGPRs: the softmax reads S directly, and the Q operands
     # are parked in AGPRs by the kernel itself
-    "anchor_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
-    "par.hip": ["-fno-signed-zeros"],
-}
+    ("anchor_attn.hip", "anchor_attn", ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]),
+    ("route_kv.hip", "route_kv", []),
+    ("capi.hip", "capi", []),
+]
 
 
 def hipcc() -> str:
@@ -42,19 +49,20 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose: bool = True, jobs: int = 4) -> str:
+def build(verbose: bool = True, jobs: int = 0) -> str:
+    jobs = jobs or max(1, min(8, os.cpu_count() or 1))
     os.makedirs(BUILD, exist_ok=True)
     cc = hipcc()
     procs = []
     objs = []
     t0 = time.time()
-    for src, extra in UNITS.items():
-        obj = os.path.join(BUILD, src.replace(".hip", ".o"))
+    for src, name, extra in UNITS:
+        obj = os.path.join(BUILD, name + ".o")
         objs.append(obj)
         cmd = [cc, "-c", os.path.join(CSRC, src), "-o", obj] + COMMON + extra
         if verbose:
             print("[build]", " ".join(cmd), flush=True)
-        procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))
+        procs.append((name, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))
         while sum(p.poll() is None for _, p in procs) >= jobs:
             time.sleep(0.05)
     failed = []

@@ -19,195 +19,24 @@
 // HBM traffic is the anchors (read by xspec and again by recon; the second read
 // is usually served by the Infinity Cache) plus the skipped frames written (or
 // read and written in accumulate mode).  Tiles are at most 8x8; every tile shape
-// (Hp, Wp) in [1,8]^2 has its own fully unrolled code path, selected per block.
-#include "cast_common.h"
-#include "fft_tile.h"
+// (Hp, Wp) in [1,8]^2 has its own fully unrolled code path.  With the default
+// 8x8 tiling each pass is one launch over all tile classes (interior, right
+// column, bottom row, corner; kernels in par_fused.hip), so small edge classes do
+// not each pay a launch and a drain; other tilings launch per class.
+#include "par_device.h"
 
 namespace cast {
 
+using namespace pardev;
+
 namespace {
-
-constexpr int kBins = kParBinsMax;     // 40 stored-bin slots: index ky*5 + kx
-constexpr int kNkx = kParNkxMax;       // 5
-constexpr int kVals = kBins * 3;       // (Re Z, Im Z, W) per slot
-constexpr int kLdsStride = kVals + 1;  // odd row stride: conflict-free LDS transpose
-constexpr int kChb = 64;               // channels per block (one wave)
-
-struct ParArgs {
-  float* theta_out;
-  float* gate_out;
-  float* conf_out;
-  long long frame_elems;  // Hg * Wg * D
-  int n_frames, Hg, Wg, D;
-  int tile_h, tile_w, n_tx, n_tiles;
-  int n_anchor, n_chblk, bins_out;
-  float tau_low, tau_high, q, T, eta_rel, eta_abs, eps;
-  int gate_mode, accumulate;
-  short anchors[kParMaxAnchors];
-};
-
-struct TileGeom {
-  int y0, x0, hp, wp;
-};
-
-__device__ __forceinline__ TileGeom tile_geom(const ParArgs& a, int tile) {
-  TileGeom g;
-  int ty = tile / a.n_tx, tx = tile - ty * a.n_tx;
-  g.y0 = ty * a.tile_h;
-  g.x0 = tx * a.tile_w;
-  g.hp = min(a.tile_h, a.Hg - g.y0);
-  g.wp = min(a.tile_w, a.Wg - g.x0);
-  return g;
-}
-
-// Tiles of one shape form a rectangle in tile coordinates (the interior, the
-// right edge column, the bottom edge row, the corner); a launch covers one.
-struct TileClass {
-  int ty0, tx0, ntx;
-};
-
-__device__ __forceinline__ int class_tile(const ParArgs& a, const TileClass& k, int b) {
-  const int r = b / k.ntx;
-  return (k.ty0 + r) * a.n_tx + k.tx0 + (b - r * k.ntx);
-}
-
-// Frame-wide buffer resource: every element access is (lane channel offset in a
-// VGPR) + (token offset, uniform across the wave, in an SGPR); accesses outside
-// the frame return 0 / are dropped by the hardware range check.
-constexpr int kBufDword3 = 0x00020000;   // 32-bit data format, gfx9-family V#
-constexpr int kNT = 2;                   // nontemporal cache policy (streaming stores)
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t frame_rsrc(const float* base, long long frame,
-                                                             long long frame_elems) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base) + frame * frame_elems, 0,
-                                           (int)(unsigned)(frame_elems * 4), kBufDword3);
-}
-__device__ __forceinline__ float buf_ld(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
-  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
-}
-template <int AUX>
-__device__ __forceinline__ void buf_st(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff,
-                                       float v) {
-  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)voff, (int)soff, AUX);
-}
-
-// A stored column kx holds its own conjugates (kx = 0, and kx = W/2 for even W).
-__host__ __device__ constexpr bool herm_col(int kx, int W) { return kx == 0 || (W % 2 == 0 && 2 * kx == W); }
-// Number of stored rows that are kept for column kx (Hermitian columns keep ky <= H/2).
-__host__ __device__ constexpr int col_rows(int kx, int H, int W) { return herm_col(kx, W) ? H / 2 + 1 : H; }
-__host__ __device__ constexpr bool self_conj(int ky, int kx, int H, int W) {
-  return herm_col(kx, W) && (ky == 0 || 2 * ky == H);
-}
-
-// Unnormalised forward 2-D real DFT of one channel of one tile, kept on the
-// unique bins only: Hermitian columns ky <= HP/2, other columns all ky.
-// `r` covers the frame, `tile0` is the byte offset of channel 0 of the tile's
-// top-left token, `c4` the lane's channel byte offset (always in range).
-template <int HP, int WP>
-__device__ __forceinline__ void load_fwd(__amdgpu_buffer_rsrc_t r, unsigned tile0, unsigned WgD4,
-                                         unsigned D4, unsigned c4, float (&fr)[HP][WP / 2 + 1],
-                                         float (&fi)[HP][WP / 2 + 1]) {
-  constexpr int NKX = WP / 2 + 1;
-  float x[HP][WP];
-  fft::static_for<0, HP>([&](auto yy) {
-    constexpr int y = decltype(yy)::value;
-    fft::static_for<0, WP>([&](auto xx) {
-      constexpr int xi = decltype(xx)::value;
-      x[y][xi] = buf_ld(r, c4, tile0 + y * WgD4 + xi * D4);
-    });
-  });
-  float rr[HP][NKX], ri[HP][NKX];
-  fft::static_for<0, HP>([&](auto yy) {
-    constexpr int y = decltype(yy)::value;
-    fft::rdft<WP>(x[y], rr[y], ri[y]);
-  });
-  fft::static_for<0, NKX>([&](auto kk) {
-    constexpr int kx = decltype(kk)::value;
-    if constexpr (herm_col(kx, WP)) {
-      float col[HP], cr[HP / 2 + 1], ci[HP / 2 + 1];
-      fft::static_for<0, HP>([&](auto yy) { col[decltype(yy)::value] = rr[decltype(yy)::value][kx]; });
-      fft::rdft<HP>(col, cr, ci);
-      fft::static_for<0, HP / 2 + 1>([&](auto yy) {
-        constexpr int ky = decltype(yy)::value;
-        fr[ky][kx] = cr[ky];
-        fi[ky][kx] = ci[ky];
-      });
-    } else {
-      float cr[HP], ci[HP];
-      fft::static_for<0, HP>([&](auto yy) {
-        constexpr int y = decltype(yy)::value;
-        cr[y] = rr[y][kx];
-        ci[y] = ri[y][kx];
-      });
-      fft::cdft<HP, false>(cr, ci);
-      fft::static_for<0, HP>([&](auto yy) {
-        constexpr int ky = decltype(yy)::value;
-        fr[ky][kx] = cr[ky];
-        fi[ky][kx] = ci[ky];
-      });
-    }
-  });
-}
-
-// ---------------------------------------------------------------------------
-// par_xspec
-// ---------------------------------------------------------------------------
-template <int HP, int WP>
-__device__ __forceinline__ void xspec_body(const ParArgs& a, const float* __restrict__ resid,
-                                           const TileGeom& g, int c_lane, int fa, int fb,
-                                           float* lds_row) {
-  constexpr int NKX = WP / 2 + 1;
-  const bool valid = c_lane < a.D;
-  const unsigned c4 = 4u * (unsigned)(valid ? c_lane : a.D - 1);
-  const unsigned tile0 = 4u * (unsigned)((g.y0 * a.Wg + g.x0) * a.D);
-  const unsigned WgD4 = 4u * (unsigned)(a.Wg * a.D), D4 = 4u * (unsigned)a.D;
-  float ar[HP][NKX], ai[HP][NKX], br[HP][NKX], bi[HP][NKX];
-  load_fwd<HP, WP>(frame_rsrc(resid, fa, a.frame_elems), tile0, WgD4, D4, c4, ar, ai);
-  load_fwd<HP, WP>(frame_rsrc(resid, fb, a.frame_elems), tile0, WgD4, D4, c4, br, bi);
-  const float live = valid ? 1.0f : 0.0f;   // lanes past D contribute nothing
-  // every slot of the lane's LDS row is written (zeros where no unique bin lives)
-  fft::static_for<0, kNkx * HP>([&](auto bb) {
-    constexpr int ky = decltype(bb)::value / kNkx;
-    constexpr int kx = decltype(bb)::value % kNkx;
-    constexpr int s = (ky * kNkx + kx) * 3;
-    if constexpr (kx < NKX && ky < col_rows(kx, HP, WP)) {
-      const float xr = ar[ky][kx], xi = ai[ky][kx], yr = br[ky][kx], yi = bi[ky][kx];
-      lds_row[s + 0] = live * (yr * xr + yi * xi);
-      lds_row[s + 1] = self_conj(ky, kx, HP, WP) ? 0.0f : live * (yi * xr - yr * xi);
-      lds_row[s + 2] = live * sqrtf((xr * xr + xi * xi) * (yr * yr + yi * yi));
-    } else {
-      lds_row[s + 0] = 0.0f;
-      lds_row[s + 1] = 0.0f;
-      lds_row[s + 2] = 0.0f;
-    }
-  });
-  for (int s = HP * kNkx * 3; s < kVals; ++s) lds_row[s] = 0.0f;
-}
 
 template <int HP, int WP>
 __global__ __launch_bounds__(64) void par_xspec_kernel(ParArgs a, TileClass k,
                                                         const float* __restrict__ resid,
                                                         float* __restrict__ partial) {
   __shared__ float lds[kChb * kLdsStride];
-  const int tile = class_tile(a, k, blockIdx.x), chb = blockIdx.y, pair = blockIdx.z;
-  const TileGeom g = tile_geom(a, tile);
-  const int lane = threadIdx.x;
-  const int c = chb * kChb + lane;
-  const int fa = a.anchors[pair], fb = a.anchors[pair + 1];
-  xspec_body<HP, WP>(a, resid, g, c, fa, fb, lds + lane * kLdsStride);
-  __syncthreads();
-  float* dst = partial + (((long long)pair * a.n_tiles + tile) * a.n_chblk + chb) * kVals;
-  for (int v = lane; v < kVals; v += kChb) {
-    float s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
-#pragma unroll 16
-    for (int l = 0; l < kChb; l += 4) {
-      s0 += lds[(l + 0) * kLdsStride + v];
-      s1 += lds[(l + 1) * kLdsStride + v];
-      s2 += lds[(l + 2) * kLdsStride + v];
-      s3 += lds[(l + 3) * kLdsStride + v];
-    }
-    dst[v] = (s0 + s1) + (s2 + s3);
-  }
+  xspec_block<HP, WP>(a, class_tile(a, k, blockIdx.x), blockIdx.y, blockIdx.z, resid, partial, lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -321,155 +150,14 @@ __global__ __launch_bounds__(64) void par_gate_kernel(ParArgs a, const float* __
   }
 }
 
-// ---------------------------------------------------------------------------
-// par_recon
-// ---------------------------------------------------------------------------
-// Number of unique stored bins of an HP x WP tile (Hermitian columns keep ky <= HP/2).
-template <int HP, int WP>
-constexpr int unique_bins() {
-  int n = 0;
-  for (int kx = 0; kx <= WP / 2; ++kx) n += col_rows(kx, HP, WP);
-  return n;
-}
-// Slot of unique bin (ky, kx) in that enumeration (column-major over kx).
-template <int HP, int WP>
-constexpr int unique_slot(int ky, int kx) {
-  int n = 0;
-  for (int c = 0; c < kx; ++c) n += col_rows(c, HP, WP);
-  return n + ky;
-}
-
-template <int HP, int WP, bool ACC>
-__device__ __forceinline__ void recon_body(const ParArgs& a, const float* __restrict__ resid,
-                                           float* __restrict__ out,
-                                           const float4* __restrict__ coef, const TileGeom& g,
-                                           int tile, int c_lane, int pair, float* fb_lds) {
-  constexpr int NKX = WP / 2 + 1;
-  constexpr int NU = unique_bins<HP, WP>();
-  // Lanes past the last channel mirror channel D-1: same inputs, same results, and
-  // they sit in the same wave as the lane that owns D-1, so their stores (and
-  // read-modify-writes) coincide with it instruction by instruction.
-  const unsigned c4 = 4u * (unsigned)(c_lane < a.D ? c_lane : a.D - 1);
-  const unsigned tile0 = 4u * (unsigned)((g.y0 * a.Wg + g.x0) * a.D);
-  const unsigned WgD4 = 4u * (unsigned)(a.Wg * a.D), D4 = 4u * (unsigned)a.D;
-  const int fa = a.anchors[pair], fb = a.anchors[pair + 1];
-  float ar[HP][NKX], ai[HP][NKX];
-  {
-    // F_b is parked in this lane's LDS column (LDS as extra per-lane storage: no
-    // other lane reads it, so no barrier is needed)
-    float br[HP][NKX], bi[HP][NKX];
-    load_fwd<HP, WP>(frame_rsrc(resid, fb, a.frame_elems), tile0, WgD4, D4, c4, br, bi);
-    fft::static_for<0, NKX>([&](auto kk) {
-      constexpr int kx = decltype(kk)::value;
-      fft::static_for<0, col_rows(kx, HP, WP)>([&](auto yy) {
-        constexpr int ky = decltype(yy)::value;
-        constexpr int u = unique_slot<HP, WP>(ky, kx);
-        fb_lds[(2 * u) * kChb] = br[ky][kx];
-        fb_lds[(2 * u + 1) * kChb] = bi[ky][kx];
-      });
-    });
-  }
-  load_fwd<HP, WP>(frame_rsrc(resid, fa, a.frame_elems), tile0, WgD4, D4, c4, ar, ai);
-  (void)NU;
-  const int n_pairs = a.n_anchor - 1;
-  for (int part = 0; part < 3; ++part) {
-    int t0, t1;
-    if (part == 0) { t0 = fa + 1; t1 = fb; }
-    else if (part == 1) { if (pair != 0) continue; t0 = 0; t1 = fa; }
-    else { if (pair != n_pairs - 1) continue; t0 = fb + 1; t1 = a.n_frames; }
-    for (int t = t0; t < t1; ++t) {
-      const float4* __restrict__ cf = coef + ((long long)t * a.n_tiles + tile) * kBins;
-      const __amdgpu_buffer_rsrc_t dst = frame_rsrc(out, t, a.frame_elems);
-      // Recompute the uniform token offsets per target instead of keeping 64 of them
-      // live across the target loop.
-      unsigned wgd = __builtin_amdgcn_readfirstlane(WgD4), dd = __builtin_amdgcn_readfirstlane(D4);
-      asm volatile("" : "+s"(wgd), "+s"(dd));
-      // likewise re-read F_b from LDS per target rather than hoisting it into VGPRs
-      const float* fbp = fb_lds;
-      asm volatile("" : "+v"(fbp));
-      // accumulate mode: fetch X_t first, all 64 loads in flight together (nothing
-      // is stored to this frame before they are issued)
-      float old[HP][WP];
-      if constexpr (ACC) {
-        fft::static_for<0, HP>([&](auto yy) {
-          constexpr int y = decltype(yy)::value;
-          fft::static_for<0, WP>([&](auto xx) {
-            constexpr int xi = decltype(xx)::value;
-            old[y][xi] = buf_ld(dst, c4, tile0 + y * wgd + xi * dd);
-          });
-        });
-      }
-      // eq:fcpasm blend and the column (y) inverse, one stored column at a time
-      float gr[HP][NKX], gi[HP][NKX];
-      fft::static_for<0, NKX>([&](auto kk) {
-        constexpr int kx = decltype(kk)::value;
-        auto fbr = [&](int u) { return fbp[(2 * u) * kChb]; };
-        auto fbi = [&](int u) { return fbp[(2 * u + 1) * kChb]; };
-        if constexpr (herm_col(kx, WP)) {
-          float hr[HP / 2 + 1], hi[HP / 2 + 1], col[HP];
-          fft::static_for<0, HP / 2 + 1>([&](auto yy) {
-            constexpr int ky = decltype(yy)::value;
-            constexpr int u = unique_slot<HP, WP>(ky, kx);
-            const float4 k = cf[ky * kNkx + kx];
-            if constexpr (self_conj(ky, kx, HP, WP)) {
-              hr[ky] = k.x * ar[ky][kx] + k.z * fbr(u);
-              hi[ky] = 0.0f;
-            } else {
-              const float b_r = fbr(u), b_i = fbi(u);
-              hr[ky] = k.x * ar[ky][kx] - k.y * ai[ky][kx] + k.z * b_r - k.w * b_i;
-              hi[ky] = k.x * ai[ky][kx] + k.y * ar[ky][kx] + k.z * b_i + k.w * b_r;
-            }
-          });
-          fft::c2r<HP>(hr, hi, col);
-          fft::static_for<0, HP>([&](auto yy) {
-            constexpr int y = decltype(yy)::value;
-            gr[y][kx] = col[y];
-            gi[y][kx] = 0.0f;
-          });
-        } else {
-          float hr[HP], hi[HP];
-          fft::static_for<0, HP>([&](auto yy) {
-            constexpr int ky = decltype(yy)::value;
-            constexpr int u = unique_slot<HP, WP>(ky, kx);
-            const float4 k = cf[ky * kNkx + kx];
-            const float b_r = fbr(u), b_i = fbi(u);
-            hr[ky] = k.x * ar[ky][kx] - k.y * ai[ky][kx] + k.z * b_r - k.w * b_i;
-            hi[ky] = k.x * ai[ky][kx] + k.y * ar[ky][kx] + k.z * b_i + k.w * b_r;
-          });
-          fft::cdft<HP, true>(hr, hi);
-          fft::static_for<0, HP>([&](auto yy) {
-            constexpr int y = decltype(yy)::value;
-            gr[y][kx] = hr[y];
-            gi[y][kx] = hi[y];
-          });
-        }
-      });
-      // row (x) inverse real transforms and the store / accumulate
-      fft::static_for<0, HP>([&](auto yy) {
-        constexpr int y = decltype(yy)::value;
-        float xv[WP];
-        fft::c2r<WP>(gr[y], gi[y], xv);
-        fft::static_for<0, WP>([&](auto xx) {
-          constexpr int xi = decltype(xx)::value;
-          const unsigned so = tile0 + y * wgd + xi * dd;
-          if constexpr (ACC) buf_st<0>(dst, c4, so, old[y][xi] + xv[xi]);
-          else buf_st<kNT>(dst, c4, so, xv[xi]);
-        });
-      });
-    }
-  }
-}
-
 template <int HP, int WP, bool ACC>
 __global__ __launch_bounds__(64) void par_recon_kernel(ParArgs a, TileClass k,
                                                         const float* __restrict__ resid,
                                                         float* __restrict__ out,
                                                         const float4* __restrict__ coef) {
   __shared__ float fb_lds[2 * kBins * kChb];
-  const int tile = class_tile(a, k, blockIdx.x), chb = blockIdx.y, pair = blockIdx.z;
-  const TileGeom g = tile_geom(a, tile);
-  recon_body<HP, WP, ACC>(a, resid, out, coef, g, tile, chb * kChb + threadIdx.x, pair,
-                          fb_lds + threadIdx.x);
+  recon_block<HP, WP, ACC>(a, class_tile(a, k, blockIdx.x), blockIdx.y, blockIdx.z, resid, out,
+                           coef, fb_lds);
 }
 
 // Host-side table of the per-shape kernels, indexed [HP-1][WP-1].
@@ -504,6 +192,24 @@ const ReconFn kReconA[8][8] = {CAST_SHAPE_ROW(1, recon_a), CAST_SHAPE_ROW(2, rec
                                CAST_SHAPE_ROW(5, recon_a), CAST_SHAPE_ROW(6, recon_a),
                                CAST_SHAPE_ROW(7, recon_a), CAST_SHAPE_ROW(8, recon_a)};
 #undef CAST_SHAPE_ROW
+
+// Table of fused-kernel rows, filled on first use (the rows live in their own
+// translation units).
+const FusedRow& fused_row(int hr) {
+  static const FusedRow* rows = [] {
+    static FusedRow r[8];
+    fused_row_1(r[0]);
+    fused_row_2(r[1]);
+    fused_row_3(r[2]);
+    fused_row_4(r[3]);
+    fused_row_5(r[4]);
+    fused_row_6(r[5]);
+    fused_row_7(r[6]);
+    fused_row_8(r[7]);
+    return r;
+  }();
+  return rows[hr - 1];
+}
 
 struct ClassLaunch {
   int hp, wp, ntiles;
@@ -575,9 +281,36 @@ cast_status_t launch_par(const float* resid, const int* anchors, int n_anchor, i
   a.accumulate = p.accumulate;
   for (int j = 0; j < n_anchor; ++j) a.anchors[j] = (short)anchors[j];
 
+  cast_status_t st;
+  if (p.tile_h == 8 && p.tile_w == 8) {
+    // default tiling: one fused launch per pass covers every tile class
+    const int nyf = Hg / 8, hr = Hg % 8, nxf = Wg / 8, wr = Wg % 8;
+    ClassSet cs{};
+    cs.k[0] = {0, 0, nxf};
+    cs.k[1] = {0, nxf, 1};
+    cs.k[2] = {nyf, 0, nxf};
+    cs.k[3] = {nyf, nxf, 1};
+    cs.end[0] = nyf * nxf;
+    cs.end[1] = cs.end[0] + (wr > 0 ? nyf : 0);
+    cs.end[2] = cs.end[1] + (hr > 0 ? nxf : 0);
+    cs.end[3] = cs.end[2] + (hr > 0 && wr > 0 ? 1 : 0);
+    const FusedRow& row = fused_row(hr > 0 ? hr : 8);
+    const int wi = (wr > 0 ? wr : 8) - 1;
+    dim3 grid(cs.end[3], pl.n_chblk, pl.n_pairs);
+    hipLaunchKernelGGL(row.xspec[wi], grid, dim3(kChb), 0, stream, a, cs, resid, partial);
+    st = check_launch("par_xspec");
+    if (st != CAST_OK) return st;
+    hipLaunchKernelGGL(par_gate_kernel, dim3(pl.n_tiles, pl.n_pairs), dim3(64), 0, stream, a,
+                       (const float*)partial, coef);
+    st = check_launch("par_gate");
+    if (st != CAST_OK) return st;
+    hipLaunchKernelGGL(p.accumulate ? row.recon_a[wi] : row.recon_w[wi], grid, dim3(kChb), 0,
+                       stream, a, cs, resid, out, (const float4*)coef);
+    return check_launch("par_recon");
+  }
+  // other tilings: one launch per tile class and pass
   ClassLaunch cls[4];
   const int ncls = tile_classes(Hg, Wg, p.tile_h, p.tile_w, cls);
-  cast_status_t st;
   for (int j = 0; j < ncls; ++j) {
     dim3 grid(cls[j].ntiles, pl.n_chblk, pl.n_pairs);
     hipLaunchKernelGGL(kXspec[cls[j].hp - 1][cls[j].wp - 1], grid, dim3(kChb), 0, stream, a,
