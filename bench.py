@@ -49,6 +49,24 @@ def par_bytes(w, accumulate=True):
     return frame * (w.n_a + n_skip * (2 if accumulate else 1))
 
 
+def load_traffic(workload):
+    """HBM bytes per call (route / attn / par) from the committed counter summary
+    profiles/hbm_traffic_<workload>.json (written by paper_2609_34144_amd.hbm_traffic
+    from rocprofv3 FETCH_SIZE / WRITE_SIZE passes); a part whose kernel sources
+    changed since the counters were taken is left out (reported as null)."""
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.json")
+    if not os.path.exists(path):
+        return {}
+    from paper_2609_34144_amd.hbm_traffic import sources_hash
+    with open(path) as fh:
+        doc = json.load(fh)
+    out = {}
+    for part, v in doc.get("per_call_bytes", {}).items():
+        if doc.get("sources", {}).get(part) == sources_hash(part):
+            out[part] = v["bytes"]
+    return out
+
+
 def cpu_baseline(w, seed=42, attn_pairs=2):
     """The oracle as it stands, timed on this host on a bounded sample of the
     workload: full routing, `attn_pairs` of the n_a*H (anchor, head) attention
@@ -199,25 +217,28 @@ def main():
         "per_call_ms": {"route": route_ms, "attn": attn_ms, "par": par_ms},
     }
     extra = {}
+    traffic = load_traffic(w.name)
     if w.has_attention:
         fl = attn_flops(w, k_eff)
         tf = fl / (attn_ms / 1e3) / 1e12
         res["roofline"] = {"bound": "mfma", "kernel": "anchor_attn_kernel<128>",
                            "achieved": tf, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                           "frac": tf / PEAK_BF16_TFLOPS, "traffic": None,
+                           "frac": tf / PEAK_BF16_TFLOPS, "traffic": traffic.get("attn"),
                            "algorithmic_per_launch": fl}
         extra["attn_mfma_util_pct"] = 100.0 * tf / PEAK_BF16_TFLOPS
         rg = route_bytes(w) / (route_ms / 1e3) / 1e9
         extra["route_hbm_gbps"] = rg
         extra["route_hbm_pct"] = 100.0 * rg / PEAK_HBM_GBS
+        extra["route_traffic_bytes"] = traffic.get("route")
     if w.has_par:
         pg = par_bytes(w, True) / (par_ms / 1e3) / 1e9
         extra["par_hbm_gbps"] = pg
         extra["par_hbm_pct"] = 100.0 * pg / PEAK_HBM_GBS
+        extra["par_traffic_bytes"] = traffic.get("par")
         if not w.has_attention:
             res["roofline"] = {"bound": "hbm", "kernel": "par (xspec+gate+recon)",
                                "achieved": pg, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                               "frac": pg / PEAK_HBM_GBS, "traffic": None,
+                               "frac": pg / PEAK_HBM_GBS, "traffic": traffic.get("par"),
                                "algorithmic_per_launch": par_bytes(w, True)}
     res.update(extra)
     if not args.no_cpu_baseline:
