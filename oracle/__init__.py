@@ -12,9 +12,11 @@ route  pooled chunk scores and TopK chunk selection   (Sec. 4.4, eq:pooled, eq:t
 attn   dense softmax attention over routed chunks     (Sec. 4.4, App. B.4 complexity)
 par    Phase-Aware Reconstruction                     (Sec. 4.3 eq:cross .. eq:fcpasm,
                                                        App. A.2, Sec. 4.1 eq:block)
+coupled  reconstruction-coupled historical routing    (Sec. 4.4 eq:omission .. eq:topk,
+                                                       App. B, Algorithm 1)
 
 Every function computes in float64 on the values it is given (bf16-rounded or
 fp32 inputs are widened first), written as the definition in the paper, with
 no blocking or fusion beyond what the definition states.
 """
-from . import route, attn, par  # noqa: F401
+from . import route, attn, par, coupled  # noqa: F401

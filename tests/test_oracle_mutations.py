@@ -11,6 +11,8 @@ import pytest
 import oracle.par as P
 import oracle.route as R
 import oracle.attn as A
+import oracle.coupled as OC
+import test_oracle_coupled as TC
 import test_oracle_par as TP
 import test_oracle_route_attn as TR
 
@@ -185,3 +187,81 @@ def test_route_mutation_caught(name):
 def test_attn_mutation_caught(name):
     mod = clone(A, **ATTN_MUTANTS[name])
     assert _any_pin_fails(mod, TR.ATTN_PINS), name
+
+
+# ---- reconstruction-coupled routing
+def _gains_no_cross(i, x, u, anchors, n_frames, l_anc=1.0, l_rec=1.0):
+    x = np.asarray(x, dtype=np.float64)
+    u = np.asarray(u, dtype=np.float64)
+    an = [int(a) for a in anchors]
+    G = l_anc * u[i].copy()
+    if i > 0:
+        G += l_rec * OC.interval_coeffs(an[i - 1], an[i])[1] * u[i]
+    if i < len(an) - 1:
+        G += l_rec * OC.interval_coeffs(an[i], an[i + 1])[0] * u[i]
+    return G
+
+
+def _boundary_signed_cross(anchors, n_frames):
+    out = OC.boundary_coeffs(anchors, n_frames)
+    res = {}
+    for q, (a, b, A_, B_, C_) in out.items():
+        ts = range(0, a) if q == "L" else range(b + 1, n_frames)
+        C2 = sum(((t - a) / (b - a)) * (1 - (t - a) / (b - a)) for t in ts)
+        res[q] = (a, b, A_, B_, C2)
+    return res
+
+
+def _omission_stab_numerator(qb, kb, vb, P_, scale, eps=1e-8):
+    _, pi, o_bar = OC.pooled_stats(qb, kb, vb, scale)
+    vb = np.asarray(vb, dtype=np.float64)
+    coef = pi / (1.0 + eps)
+    delta = coef[:, :, None] * (o_bar[:, None, :] - vb[None, :, :])
+    proj = np.einsum("dk,imk->imd", np.asarray(P_, np.float64), delta)
+    return (proj ** 2).sum(axis=2), delta
+
+
+def _omission_transposed_proj(qb, kb, vb, P_, scale, eps=1e-8):
+    u, delta = OC.omission(qb, kb, vb, P_, scale, eps)
+    return (delta ** 2).sum(axis=2) * float((np.asarray(P_) ** 2).mean()), delta
+
+
+def _gains_boundary_swapped(i, x, u, anchors, n_frames, l_anc=1.0, l_rec=1.0):
+    G = OC.gains(i, x, u, anchors, n_frames, l_anc, l_rec)
+    an = [int(a) for a in anchors]
+    row = {a: r for r, a in enumerate(an)}
+    for (a, b, A_, B_, C_) in OC.boundary_coeffs(an, n_frames).values():
+        if i == row[a]:
+            G += l_rec * (B_ - A_) * np.asarray(u, np.float64)[i]
+    return G
+
+
+COUPLED_MUTANTS = {
+    "gain_no_cross_term": dict(gains=_gains_no_cross),
+    "boundary_signed_cross": dict(boundary_coeffs=_boundary_signed_cross),
+    "omission_stabiliser_numerator": dict(omission=_omission_stab_numerator),
+    "omission_projection_ignored": dict(omission=_omission_transposed_proj),
+    "gain_boundary_A_B_swapped": dict(gains=_gains_boundary_swapped),
+}
+
+
+@pytest.mark.parametrize("name", sorted(COUPLED_MUTANTS))
+def test_coupled_mutation_caught(name):
+    mod = clone(OC, **COUPLED_MUTANTS[name])
+    assert _any_pin_fails(mod, TC.PINS), name
+
+
+def test_coupled_refine_mutations_caught():
+    """Accepting ties (no strict decrease) and a forward-only second pass are caught
+    by the hand-worked coupling example's trace."""
+    src = OC.refine.__code__
+    import inspect
+    text = inspect.getsource(OC.refine)
+    for bad in (text.replace("(g_new - g_old) > tol * max(J, 1e-8)", "(g_new - g_old) >= 0.0"),
+                text.replace("if s % 2 == 0 else range(n_a - 1, -1, -1)", "")):
+        assert bad != text
+        ns = dict(OC.__dict__)
+        exec(compile(bad, "<mutant>", "exec"), ns)
+        mod = clone(OC, refine=ns["refine"])
+        assert _any_pin_fails(mod, TC.PINS)
+    del src
