@@ -41,6 +41,12 @@ def route_bytes(w):
     return 2.0 * (w.M * w.Bv + w.n_a * w.S) * w.H * w.dh
 
 
+def coupled_route_bytes(w):
+    """Algorithmic bytes of coupled routing: one read of K and V history and of the
+    anchor Q (bf16); the solver's own traffic is negligible."""
+    return 2.0 * (2 * w.M * w.Bv + w.n_a * w.S) * w.H * w.dh
+
+
 def par_bytes(w, accumulate=True):
     """Algorithmic bytes of PAR: anchors read once; skipped frames written, and read
     too when accumulating (fp32)."""
@@ -203,6 +209,31 @@ def main():
     attn_ms = float(np.mean([m[1].elapsed_time(m[2]) for m in marks]))
     par_ms = float(np.mean([m[2].elapsed_time(m[3]) for m in marks]))
 
+    # reconstruction-coupled routing (NEXT-1), timed on its own after the step;
+    # the W_O Gram matrices depend on weights only and are prepared once, untimed
+    coupled_ms = None
+    if w.has_attention and w.M > 0:
+        gram = cast.cast_wo_gram(gen.wo_weight(w.D, device=dev), w.H, w.dh)
+        cprm = cast.cast_coupled_params_default()
+        nb = cast.cast_route_coupled_workspace_bytes(w.n_a, w.S, w.H, w.dh, w.M, w.Bv)
+        cws = torch.empty(nb, dtype=torch.uint8, device=dev)
+        cidx = torch.empty((w.n_a, w.H, k_eff), dtype=torch.int32, device=dev)
+        n_frames_c = max(w.n_frames, max(w.anchors) + 1)
+        for i in range(args.warmup):
+            s = sets[i % N_COPIES]
+            cast.cast_route_coupled(s["q"], s["k"], s["v"], gram, w.anchors, n_frames_c, w.topk,
+                                    w.scale, params=cprm, idx_out=cidx, workspace=cws, stream=stream)
+        cm = [[ev(), ev()] for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        for i in range(args.steps):
+            s = sets[i % N_COPIES]
+            cm[i][0].record(stream)
+            cast.cast_route_coupled(s["q"], s["k"], s["v"], gram, w.anchors, n_frames_c, w.topk,
+                                    w.scale, params=cprm, idx_out=cidx, workspace=cws, stream=stream)
+            cm[i][1].record(stream)
+        torch.cuda.synchronize()
+        coupled_ms = float(np.mean([a.elapsed_time(b) for a, b in cm]))
+
     value = w.frame_tokens / (ms_step / 1e3)
     res = {
         "metric": "CAST block-step frame-tokens/s (routing + routed anchor attention + PAR)",
@@ -214,7 +245,8 @@ def main():
                    "D": w.D, "heads": w.H, "dh": w.dh, "anchors": list(w.anchors),
                    "history_chunks": w.M, "chunk_tokens": w.Bv, "topk": w.topk,
                    "par_mode": "accumulate", "input_copies": N_COPIES},
-        "per_call_ms": {"route": route_ms, "attn": attn_ms, "par": par_ms},
+        "per_call_ms": {"route": route_ms, "attn": attn_ms, "par": par_ms,
+                        "route_coupled": coupled_ms},
     }
     extra = {}
     traffic = load_traffic(w.name)
@@ -230,6 +262,10 @@ def main():
         extra["route_hbm_gbps"] = rg
         extra["route_hbm_pct"] = 100.0 * rg / PEAK_HBM_GBS
         extra["route_traffic_bytes"] = traffic.get("route")
+        if coupled_ms:
+            cg = coupled_route_bytes(w) / (coupled_ms / 1e3) / 1e9
+            extra["route_coupled_hbm_gbps"] = cg
+            extra["route_coupled_hbm_pct"] = 100.0 * cg / PEAK_HBM_GBS
     if w.has_par:
         pg = par_bytes(w, True) / (par_ms / 1e3) / 1e9
         extra["par_hbm_gbps"] = pg

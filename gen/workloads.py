@@ -171,6 +171,13 @@ def attn_inputs(w: Workload, seed: int = 42, device="cpu", M=None, Bv=None,
     return q, k, v, kc, vc
 
 
+def wo_weight(D: int, seed: int = 7, device="cpu"):
+    """A synthetic attention output projection W_O, bf16 [D, D] with N(0, 1/D)
+    entries (a randomly initialised linear layer; the trained one is unavailable)."""
+    import torch
+    return (_randn((D, D), seeds_for(seed, 1)[0], device) / float(np.sqrt(D))).to(torch.bfloat16)
+
+
 # ----------------------------------------------------------------------------
 # Residual fields (fp32)
 # ----------------------------------------------------------------------------

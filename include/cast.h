@@ -107,6 +107,78 @@ cast_status_t cast_route_kv(const void* q, const void* k_hist,
                             hipStream_t stream);
 
 /* ------------------------------------------------------------------------- */
+/* Reconstruction-coupled routing (Sec. 4.4 eq:omission..eq:topk; App. B:    */
+/* eq:gain, eq:boundarygain, Algorithm 1; tab:config routing weights)        */
+/* ------------------------------------------------------------------------- */
+
+typedef struct {
+  float l_anc, l_rec;   /* objective weights lambda_anc, lambda_rec (1, 1)          */
+  int passes;           /* directional refinement passes L_s (2): forward, backward */
+  float tol;            /* accept a change when J falls by > tol * max(J, 1e-8)
+                           (1e-6)                                                   */
+  float eps;            /* stabiliser of the omission proxy, eq:omission (1e-8)     */
+} cast_coupled_params_t;
+
+/* Fill *p with the defaults above.  NULL is ignored. */
+void cast_coupled_params_default(cast_coupled_params_t* p);
+
+/*
+ * Gram matrices of the per-head output-projection slices, for the omission
+ * proxy u = ||P_h delta||^2 = delta^T (P_h^T P_h) delta (eq:omission, P_h = the
+ * head's slice of W_O).  They depend on the weights only: compute once per model.
+ *   gram[h, a, b] = sum_r w_o[r, h*dh + a] * w_o[r, h*dh + b]   (fp32 accumulation)
+ * w_o       bf16 [D, D] device, row-major, out = w_o @ concat_h(head outputs),
+ *           D = H * dh.
+ * gram_out  fp32 [H, dh, dh] device.
+ * H>=1, dh in {32, 64, 128}, H*dh == D.
+ */
+cast_status_t cast_wo_gram(const void* w_o, int D, int H, int dh, float* gram_out,
+                           hipStream_t stream);
+
+/* Device scratch (bytes) needed by cast_route_coupled for these sizes. */
+size_t cast_route_coupled_workspace_bytes(int n_a, int S, int H, int dh, int M, int Bv);
+
+/*
+ * Historical KV masks that couple neighbouring anchors through the frames they
+ * reconstruct, per head h (masks of different heads never interact):
+ *
+ *   q_bar, k_bar, v_bar = token means (fp32) of q[i,:,h,:], k_hist[m,:,h,:],
+ *                         v_hist[m,:,h,:];
+ *   s[i,m] = scale q_bar[i].k_bar[m]; pi[i,:] = softmax over the M blocks;
+ *   o_bar[i] = sum_m pi[i,m] v_bar[m];
+ *   u[i,m] = (pi/(1-pi+eps))^2 (o_bar[i]-v_bar[m])^T gram[h] (o_bar[i]-v_bar[m])
+ *                                                                (eq:omission)
+ *   masks start as TopK_m(u[i,:]) and go through `passes` directional passes of
+ *   Algorithm 1: anchor i's mask becomes TopK_m(G[i,:]) (eq:gain with the
+ *   interval coefficients of eq:abc between adjacent anchors and the boundary
+ *   coefficients of eq:boundarycoeff for frames before the first / after the
+ *   last anchor, extrapolated from the first / last pair) when that lowers the
+ *   head's objective J (eq:objective) by more than tol * max(J, 1e-8); a pass
+ *   without a change ends the refinement.
+ *
+ * TopK orders (value descending, block index ascending); idx lists each mask in
+ * ASCENDING block order, exactly k_eff = min(topk, M) blocks per (anchor, head),
+ * the layout cast_anchor_attn takes.
+ *
+ * q        bf16 [n_a, S, H, dh] device (the anchor frames).
+ * k_hist, v_hist  bf16 [M, Bv, H, dh] device.
+ * gram     fp32 [H, dh, dh] device (cast_wo_gram).
+ * anchors  HOST int [n_a], frame index of each row of q, strictly increasing,
+ *          all in [0, n_frames); 1 <= n_a <= 512, n_a * M <= 32768.
+ * u_out    fp32 [n_a, H, M] device, or NULL to skip.
+ * idx_out  int32 [n_a, H, k_eff] device (may be NULL only when M == 0).
+ * k_eff_out  HOST int, receives k_eff (required).
+ * M == 0: k_eff = 0, nothing is enqueued.  topk >= M: every block is kept (the
+ * refinement cannot change a full mask) but u is still computed.
+ */
+cast_status_t cast_route_coupled(const void* q, const void* k_hist, const void* v_hist,
+                                 const float* gram, const int* anchors,
+                                 int n_a, int n_frames, int S, int H, int dh, int M, int Bv,
+                                 int topk, float scale, const cast_coupled_params_t* params,
+                                 float* u_out, int32_t* idx_out, int* k_eff_out,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------- */
 /* Routed block-sparse anchor attention (Sec. 4.4; App. B.4 complexity)      */
 /* ------------------------------------------------------------------------- */
 

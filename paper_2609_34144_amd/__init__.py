@@ -23,7 +23,9 @@ STATUS_NAMES = {0: "CAST_OK", 1: "CAST_ERR_NULL", 2: "CAST_ERR_SHAPE", 3: "CAST_
 
 EXPORTED = ["cast_status_string", "cast_last_error_detail", "cast_abi_version",
             "cast_route_kv_workspace_bytes", "cast_route_kv", "cast_anchor_attn",
-            "cast_par_params_default", "cast_par_workspace_bytes", "cast_par_reconstruct"]
+            "cast_par_params_default", "cast_par_workspace_bytes", "cast_par_reconstruct",
+            "cast_coupled_params_default", "cast_wo_gram", "cast_route_coupled_workspace_bytes",
+            "cast_route_coupled"]
 
 
 class CastError(RuntimeError):
@@ -41,6 +43,12 @@ class ParParams(ctypes.Structure):
                 ("eta_rel", ctypes.c_float), ("eta_abs", ctypes.c_float),
                 ("eps", ctypes.c_float), ("gate_mode", ctypes.c_int),
                 ("accumulate", ctypes.c_int)]
+
+
+class CoupledParams(ctypes.Structure):
+    """cast_coupled_params_t (include/cast.h)."""
+    _fields_ = [("l_anc", ctypes.c_float), ("l_rec", ctypes.c_float),
+                ("passes", ctypes.c_int), ("tol", ctypes.c_float), ("eps", ctypes.c_float)]
 
 
 _lib = None
@@ -77,6 +85,16 @@ def load(path: str = LIB_PATH):
     lib.cast_par_reconstruct.restype = _i
     lib.cast_par_reconstruct.argtypes = [_vp, _c.POINTER(_i), _i, _i, _i, _i, _i,
                                          _c.POINTER(ParParams), _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.cast_coupled_params_default.restype = None
+    lib.cast_coupled_params_default.argtypes = [_c.POINTER(CoupledParams)]
+    lib.cast_wo_gram.restype = _i
+    lib.cast_wo_gram.argtypes = [_vp, _i, _i, _i, _vp, _vp]
+    lib.cast_route_coupled_workspace_bytes.restype = _sz
+    lib.cast_route_coupled_workspace_bytes.argtypes = [_i] * 6
+    lib.cast_route_coupled.restype = _i
+    lib.cast_route_coupled.argtypes = [_vp, _vp, _vp, _vp, _c.POINTER(_i), _i, _i, _i, _i, _i, _i,
+                                       _i, _i, _f, _c.POINTER(CoupledParams), _vp, _vp,
+                                       _c.POINTER(_i), _vp, _sz, _vp]
     _lib = lib
     return lib
 
@@ -150,6 +168,57 @@ def cast_route_kv(q, k_hist, topk: int, scale: float = 1.0, scores_out=None, idx
                              _ptr(scores_out), _ptr(idx_out), ctypes.byref(k_eff), _ptr(ws), wsb,
                              _stream(stream)))
     return idx_out, k_eff.value, scores_out
+
+
+def cast_coupled_params_default(**overrides) -> CoupledParams:
+    p = CoupledParams()
+    load().cast_coupled_params_default(ctypes.byref(p))
+    for k, v in overrides.items():
+        setattr(p, k, v)
+    return p
+
+
+def cast_route_coupled_workspace_bytes(n_a, S, H, dh, M, Bv) -> int:
+    return load().cast_route_coupled_workspace_bytes(n_a, S, H, dh, M, Bv)
+
+
+def cast_wo_gram(w_o, H: int, dh: int, gram_out=None, stream=None):
+    """Gram matrices fp32 [H, dh, dh] of the head slices of w_o bf16 [D, D] (device)."""
+    import torch
+    lib = load()
+    D = w_o.shape[0]
+    if gram_out is None:
+        gram_out = torch.empty((H, dh, dh), dtype=torch.float32, device=w_o.device)
+    _check(lib.cast_wo_gram(_ptr(w_o), D, H, dh, _ptr(gram_out), _stream(stream)))
+    return gram_out
+
+
+def cast_route_coupled(q, k_hist, v_hist, gram, anchors, n_frames: int, topk: int,
+                       scale: float, params: CoupledParams | None = None, u_out=None,
+                       idx_out=None, workspace=None, stream=None, want_u: bool = False):
+    """Reconstruction-coupled routing.  q bf16 [n_a, S, H, dh]; k_hist, v_hist bf16
+    [M, Bv, H, dh]; gram fp32 [H, dh, dh] (device); `anchors` the host frame index
+    of each row of q.  Returns (idx int32 [n_a, H, k_eff], k_eff, u fp32 [n_a, H, M]
+    or None)."""
+    import torch
+    lib = load()
+    if params is None:
+        params = cast_coupled_params_default()
+    n_a, S, H, dh = q.shape
+    M, Bv = k_hist.shape[0], k_hist.shape[1]
+    if idx_out is None and M > 0:
+        idx_out = torch.empty((n_a, H, min(topk, M)), dtype=torch.int32, device=q.device)
+    if u_out is None and want_u and M > 0:
+        u_out = torch.empty((n_a, H, M), dtype=torch.float32, device=q.device)
+    anc = [int(a) for a in anchors]
+    arr = (ctypes.c_int * max(len(anc), 1))(*anc)
+    ws, wsb = _ws(lib.cast_route_coupled_workspace_bytes(n_a, S, H, dh, M, Bv), q.device, workspace)
+    k_eff = ctypes.c_int(-1)
+    _check(lib.cast_route_coupled(_ptr(q), _ptr(k_hist), _ptr(v_hist), _ptr(gram), arr, n_a,
+                                  n_frames, S, H, dh, M, Bv, topk, scale, ctypes.byref(params),
+                                  _ptr(u_out), _ptr(idx_out), ctypes.byref(k_eff), _ptr(ws), wsb,
+                                  _stream(stream)))
+    return idx_out, k_eff.value, u_out
 
 
 def cast_anchor_attn(q, k_hist, v_hist, idx, k_eff: int, scale: float, k_cur=None, v_cur=None,

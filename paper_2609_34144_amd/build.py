@@ -38,6 +38,7 @@ UNITS = [("par.hip", "par", ["-fno-signed-zeros"])] + [
     # are parked in AGPRs by the kernel itself
     ("anchor_attn.hip", "anchor_attn", ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]),
     ("route_kv.hip", "route_kv", []),
+    ("route_coupled.hip", "route_coupled", []),
     ("capi.hip", "capi", []),
 ]
 

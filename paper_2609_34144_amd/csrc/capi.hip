@@ -105,6 +105,77 @@ cast_status_t cast_route_kv(const void* q, const void* k_hist, int n_a, int S, i
   return CAST_OK;
 }
 
+// ------------------------------------------------- coupled routing (NEXT)
+
+void cast_coupled_params_default(cast_coupled_params_t* p) {
+  if (p == nullptr) return;
+  p->l_anc = 1.0f;
+  p->l_rec = 1.0f;
+  p->passes = 2;
+  p->tol = 1e-6f;
+  p->eps = 1e-8f;
+}
+
+cast_status_t cast_wo_gram(const void* w_o, int D, int H, int dh, float* gram_out,
+                           hipStream_t stream) {
+  if (H < 1 || !dh_ok(dh) || (long long)H * dh != D)
+    return fail(CAST_ERR_SHAPE, "wo_gram: need H>=1, dh in {32,64,128}, D == H*dh (got %d %d %d)",
+                D, H, dh);
+  if ((long long)D * D >= (1LL << 31))
+    return fail(CAST_ERR_UNSUPPORTED, "wo_gram: D*D must stay below 2^31");
+  if (w_o == nullptr || gram_out == nullptr) return fail(CAST_ERR_NULL, "wo_gram: null pointer");
+  if (!aligned(w_o, 16) || !aligned(gram_out, 16))
+    return fail(CAST_ERR_SHAPE, "wo_gram: pointers must be 16-byte aligned");
+  return launch_wo_gram(w_o, D, H, dh, gram_out, stream);
+}
+
+size_t cast_route_coupled_workspace_bytes(int n_a, int S, int H, int dh, int M, int Bv) {
+  if (route_shape_check(n_a, S, H, dh, M, Bv) != CAST_OK || M == 0) return 0;
+  return plan_coupled(n_a, S, H, dh, M, Bv).total;
+}
+
+cast_status_t cast_route_coupled(const void* q, const void* k_hist, const void* v_hist,
+                                 const float* gram, const int* anchors, int n_a, int n_frames,
+                                 int S, int H, int dh, int M, int Bv, int topk, float scale,
+                                 const cast_coupled_params_t* params, float* u_out,
+                                 int32_t* idx_out, int* k_eff_out, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream) {
+  if (k_eff_out == nullptr) return fail(CAST_ERR_NULL, "coupled: k_eff_out is NULL");
+  cast_status_t st = route_shape_check(n_a, S, H, dh, M, Bv);
+  if (st != CAST_OK) return st;
+  if (topk < 1) return fail(CAST_ERR_SHAPE, "coupled: topk must be >= 1 (got %d)", topk);
+  if (params == nullptr) return fail(CAST_ERR_NULL, "coupled: params is NULL");
+  if (!(params->l_anc >= 0.0f) || !(params->l_rec >= 0.0f) || !(params->tol >= 0.0f) ||
+      !(params->eps >= 0.0f) || params->passes < 0 || params->passes > 1000)
+    return fail(CAST_ERR_SHAPE, "coupled: weights, tol, eps must be >= 0 and 0 <= passes <= 1000");
+  if (anchors == nullptr) return fail(CAST_ERR_NULL, "coupled: anchors is NULL");
+  if (n_a > kCoupledMaxAnchors)
+    return fail(CAST_ERR_UNSUPPORTED, "coupled: n_a=%d exceeds %d anchors", n_a, kCoupledMaxAnchors);
+  if (n_frames < n_a || n_frames > 32767)
+    return fail(CAST_ERR_SHAPE, "coupled: n_frames=%d must be in [n_a, 32767]", n_frames);
+  for (int j = 0; j < n_a; ++j) {
+    if (anchors[j] < 0 || anchors[j] >= n_frames || (j > 0 && anchors[j] <= anchors[j - 1]))
+      return fail(CAST_ERR_ANCHORS, "coupled: anchors must be strictly increasing in [0, n_frames)");
+  }
+  if (M == 0) { *k_eff_out = 0; return CAST_OK; }
+  if ((long long)n_a * M > kCoupledMaxMask)
+    return fail(CAST_ERR_UNSUPPORTED, "coupled: n_a*M=%lld exceeds %d", (long long)n_a * M,
+                kCoupledMaxMask);
+  if (q == nullptr || k_hist == nullptr || v_hist == nullptr || gram == nullptr || idx_out == nullptr)
+    return fail(CAST_ERR_NULL, "coupled: q, k_hist, v_hist, gram and idx_out are required");
+  if (!aligned(q, 16) || !aligned(k_hist, 16) || !aligned(v_hist, 16) || !aligned(gram, 16))
+    return fail(CAST_ERR_SHAPE, "coupled: q, k_hist, v_hist, gram must be 16-byte aligned");
+  CoupledPlan plan = plan_coupled(n_a, S, H, dh, M, Bv);
+  st = check_ws(workspace, workspace_bytes, plan.total);
+  if (st != CAST_OK) return st;
+  const int k_eff = topk < M ? topk : M;
+  st = launch_coupled(q, k_hist, v_hist, gram, anchors, n_a, n_frames, S, H, dh, M, Bv, k_eff,
+                      scale, *params, u_out, idx_out, plan, workspace, stream);
+  if (st != CAST_OK) return st;
+  *k_eff_out = k_eff;
+  return CAST_OK;
+}
+
 // ---------------------------------------------------------------- attention
 
 cast_status_t cast_anchor_attn(const void* q, const void* k_hist, const void* v_hist,

@@ -42,9 +42,35 @@ constexpr int kRouteMaxM = 4096;   // bitonic keys live in 32 KB of LDS
 
 RoutePlan plan_route(int n_a, int S, int H, int dh, int M, int Bv);
 
+// Pooled means of n_a frames of q (S tokens) and M chunks of k (Bv tokens):
+// means [n_a + M, D] fp32 (q_bar rows first).  n_a may be 0.
+cast_status_t launch_pool_means(const void* q, const void* k, int n_a, int S, int M, int Bv,
+                                const RoutePlan& p, float* partial, float* means,
+                                hipStream_t stream);
+
 cast_status_t launch_route(const void* q, const void* k, int n_a, int S, int H, int dh, int M,
                            int Bv, int k_eff, float scale, float* scores_out, int32_t* idx_out,
                            const RoutePlan& plan, void* ws, hipStream_t stream);
+
+// ---------------------------------------------------------------------------
+// Reconstruction-coupled routing
+// ---------------------------------------------------------------------------
+constexpr int kCoupledMaxAnchors = 512;
+constexpr int kCoupledMaxMask = 32768;   // n_a * M retain flags held in LDS by the solver
+
+struct CoupledPlan {
+  RoutePlan qk, v;      // pooled-mean scans of (Q, K) and of V
+  size_t off_partial, off_means_qk, off_means_v, off_u, total;
+};
+CoupledPlan plan_coupled(int n_a, int S, int H, int dh, int M, int Bv);
+
+cast_status_t launch_coupled(const void* q, const void* k, const void* v, const float* gram,
+                             const int* anchors, int n_a, int n_frames, int S, int H, int dh,
+                             int M, int Bv, int k_eff, float scale, const cast_coupled_params_t& prm,
+                             float* u_out, int32_t* idx_out, const CoupledPlan& plan, void* ws,
+                             hipStream_t stream);
+
+cast_status_t launch_wo_gram(const void* w_o, int D, int H, int dh, float* gram, hipStream_t stream);
 
 // ---------------------------------------------------------------------------
 // Attention

@@ -177,12 +177,10 @@ RoutePlan plan_route(int n_a, int S, int H, int dh, int M, int Bv) {
   return p;
 }
 
-cast_status_t launch_route(const void* q, const void* k, int n_a, int S, int H, int dh, int M,
-                           int Bv, int k_eff, float scale, float* scores_out, int32_t* idx_out,
-                           const RoutePlan& p, void* ws, hipStream_t stream) {
-  float* partial = reinterpret_cast<float*>(static_cast<char*>(ws) + p.off_partial);
-  float* means = reinterpret_cast<float*>(static_cast<char*>(ws) + p.off_means);
-  if (p.items > 0x7fffffff) return fail(CAST_ERR_UNSUPPORTED, "route: too many scan blocks");
+cast_status_t launch_pool_means(const void* q, const void* k, int n_a, int S, int M, int Bv,
+                                const RoutePlan& p, float* partial, float* means,
+                                hipStream_t stream) {
+  if (p.items <= 0) return CAST_OK;
   hipLaunchKernelGGL(route_pool_kernel, dim3(p.items, p.ngrp), dim3(kPoolThreads), 0, stream,
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), n_a, S, Bv,
                      p.D, p.spq, p.tq, p.spk, p.tk, partial);
@@ -190,7 +188,15 @@ cast_status_t launch_route(const void* q, const void* k, int n_a, int S, int H, 
   if (st != CAST_OK) return st;
   hipLaunchKernelGGL(route_finalize_kernel, dim3((p.D + 255) / 256, n_a + M), dim3(256), 0, stream,
                      partial, n_a, p.D, p.spq, p.spk, S, Bv, means);
-  st = check_launch("route_finalize");
+  return check_launch("route_finalize");
+}
+
+cast_status_t launch_route(const void* q, const void* k, int n_a, int S, int H, int dh, int M,
+                           int Bv, int k_eff, float scale, float* scores_out, int32_t* idx_out,
+                           const RoutePlan& p, void* ws, hipStream_t stream) {
+  float* partial = reinterpret_cast<float*>(static_cast<char*>(ws) + p.off_partial);
+  float* means = reinterpret_cast<float*>(static_cast<char*>(ws) + p.off_means);
+  cast_status_t st = launch_pool_means(q, k, n_a, S, M, Bv, p, partial, means, stream);
   if (st != CAST_OK) return st;
   int P = 2;
   while (P < M) P <<= 1;

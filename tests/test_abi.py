@@ -164,3 +164,60 @@ def test_workspace_queries_grow_with_size(lib):
     big = lib.cast_par_workspace_bytes(66, 2, 64, 64, 3072, ctypes.byref(p))
     assert 0 < small < big
     assert big % 256 == 0
+
+
+# ---- reconstruction-coupled routing
+def test_coupled_params_default_matches_paper(lib):
+    """tab:config: (lambda_anc, lambda_rec) = (1, 1), L_s = 2 passes, accept a
+    decrease > 1e-6 max(J, 1e-8); stabiliser 1e-8 (reading)."""
+    p = cast.cast_coupled_params_default()
+    assert (p.l_anc, p.l_rec, p.passes) == (1.0, 1.0, 2)
+    assert abs(p.tol - 1e-6) < 1e-12 and abs(p.eps - 1e-8) < 1e-14
+
+
+def _coupled(lib, *, q=A, k=2 * A, v=3 * A, gram=4 * A, anchors=(0, 3, 7), n_frames=8, S=64, H=2,
+             dh=32, M=4, Bv=64, topk=2, idx=5 * A, keff=True, ws=None, wsb=0, params=True, **prm):
+    p = cast.cast_coupled_params_default(**prm)
+    arr = (ctypes.c_int * max(len(anchors), 1))(*anchors) if anchors is not None else None
+    k_eff = ctypes.c_int(-7)
+    n_a = len(anchors) if anchors is not None else 3
+    st = lib.cast_route_coupled(q, k, v, gram, arr, n_a, n_frames, S, H, dh, M, Bv,
+                                topk, 0.5, ctypes.byref(p) if params else None, None, idx,
+                                ctypes.byref(k_eff) if keff else None, ws, wsb, None)
+    return st, k_eff.value
+
+
+def test_coupled_validation(lib):
+    assert _coupled(lib, keff=False)[0] == NULL
+    assert _coupled(lib, params=False)[0] == NULL
+    assert _coupled(lib, anchors=None)[0] == NULL
+    assert _coupled(lib, anchors=(0, 3, 3))[0] == ANCHORS
+    assert _coupled(lib, anchors=(0, 3, 8))[0] == ANCHORS            # outside [0, n_frames)
+    assert _coupled(lib, anchors=(2, 1, 5))[0] == ANCHORS
+    assert _coupled(lib, n_frames=2)[0] == SHAPE                     # fewer frames than anchors
+    assert _coupled(lib, dh=48)[0] == UNSUPPORTED
+    assert _coupled(lib, topk=0)[0] == SHAPE
+    assert _coupled(lib, l_anc=-1.0)[0] == SHAPE
+    assert _coupled(lib, passes=-1)[0] == SHAPE
+    assert _coupled(lib, tol=float("nan"))[0] == SHAPE
+    assert _coupled(lib, gram=None)[0] == NULL
+    assert _coupled(lib, v=None)[0] == NULL
+    assert _coupled(lib, v=A + 8)[0] == SHAPE                        # misaligned
+    assert _coupled(lib, M=20000, anchors=(0, 1, 2), n_frames=3)[0] == UNSUPPORTED
+    assert _coupled(lib, ws=None, wsb=0)[0] == WORKSPACE
+    need = lib.cast_route_coupled_workspace_bytes(3, 64, 2, 32, 4, 64)
+    assert need > lib.cast_route_kv_workspace_bytes(3, 64, 2, 32, 4, 64)
+    assert _coupled(lib, ws=6 * A, wsb=need - 1)[0] == WORKSPACE
+
+
+def test_coupled_bypass_m0(lib):
+    st, k_eff = _coupled(lib, q=None, k=None, v=None, gram=None, idx=None, M=0)
+    assert st == OK and k_eff == 0
+    assert lib.cast_route_coupled_workspace_bytes(3, 64, 2, 32, 0, 64) == 0
+
+
+def test_wo_gram_validation(lib):
+    assert lib.cast_wo_gram(A, 64, 2, 48, 2 * A, None) == SHAPE      # dh unsupported
+    assert lib.cast_wo_gram(A, 60, 2, 32, 2 * A, None) == SHAPE      # D != H * dh
+    assert lib.cast_wo_gram(None, 64, 2, 32, 2 * A, None) == NULL
+    assert lib.cast_wo_gram(A + 4, 64, 2, 32, 2 * A, None) == SHAPE
