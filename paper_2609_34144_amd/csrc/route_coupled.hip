@@ -23,6 +23,7 @@ namespace {
 
 constexpr int kOmM = 16;          // blocks per omission workgroup (4 per wave)
 constexpr int kThreads = 256;
+constexpr int kRefineThreads = 64;   // the solver runs in one wave per head
 
 struct CoupledArgs {
   const float* means_qk;   // [n_a + M, D]: q_bar rows, then k_bar rows
@@ -50,6 +51,13 @@ __device__ float block_sum(float v, float* red) {
   return r;
 }
 
+// Sum over the 64 lanes of a wave by a fixed butterfly: every lane gets the same
+// (order-independent of the schedule) result.
+__device__ __forceinline__ float wave_sum(float v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
 __device__ float block_max(float v, float* red) {
   red[threadIdx.x] = v;
   __syncthreads();
@@ -72,22 +80,24 @@ __global__ __launch_bounds__(kThreads) void coupled_omission_kernel(CoupledArgs 
   float* qs = e + a.M;         // [DH]
   float* ob = qs + DH;         // [DH]
   float* red = ob + DH;        // [kThreads]
-  float* dv = red + kThreads;  // [4][DH] one difference vector per wave
+  float* dv = red + kThreads;  // [kOmM][DH] difference vectors, kOmM / 4 per wave
   const int ih = blockIdx.x, i = ih / a.H, h = ih - (ih / a.H) * a.H;
   const int m0 = blockIdx.y * kOmM;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   for (int d = tid; d < DH; d += kThreads) qs[d] = a.means_qk[(long long)i * a.D + h * DH + d];
   __syncthreads();
+  // scores: one wave per block, lanes over the channels
   float lmax = -INFINITY;
-  for (int m = tid; m < a.M; m += kThreads) {
+  for (int m = wave; m < a.M; m += kThreads / 64) {
     const float* kb = a.means_qk + (long long)(a.n_a + m) * a.D + h * DH;
     float s = 0.0f;
-#pragma unroll 8
-    for (int d = 0; d < DH; ++d) s = fmaf(qs[d], kb[d], s);
+    for (int d = lane; d < DH; d += 64) s = fmaf(qs[d], kb[d], s);
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
     s *= a.scale;
-    e[m] = s;
+    if (lane == 0) e[m] = s;
     lmax = fmaxf(lmax, s);
   }
+  __syncthreads();
   const float smax = block_max(lmax, red);
   float lsum = 0.0f;
   for (int m = tid; m < a.M; m += kThreads) {
@@ -113,47 +123,59 @@ __global__ __launch_bounds__(kThreads) void coupled_omission_kernel(CoupledArgs 
     }
     __syncthreads();
   }
-  // u for the blocks of this range: wave w takes m0 + w, m0 + w + 4, ...
+  // u for the blocks of this range: wave w takes the 4 blocks m0 + 4w .. +3 at
+  // once, so every G element loaded serves 4 difference vectors
+  constexpr int MW = kOmM / 4;
   const float* G = a.gram + (long long)h * DH * DH;   // symmetric: row l of column c = G[c][l]
-  float* dw = dv + wave * DH;
-  for (int r = 0; r < kOmM / 4; ++r) {
-    const int m = m0 + 4 * r + wave;
-    const bool valid = m < a.M;
-    if (valid)
-      for (int c = lane; c < DH; c += 64) dw[c] = ob[c] - a.means_v[(long long)m * a.D + h * DH + c];
-    __syncthreads();
-    if (valid) {
-      float y1 = 0.0f, y2 = 0.0f;
-#pragma unroll 8
-      for (int c = 0; c < DH; ++c) {
-        const float dc = dw[c];
-        if (lane < DH) y1 = fmaf(G[c * DH + lane], dc, y1);
-        if (DH > 64) y2 = fmaf(G[c * DH + lane + 64], dc, y2);
-      }
-      float part = lane < DH ? dw[lane] * y1 : 0.0f;
-      if (DH > 64) part += dw[lane + 64] * y2;
-      for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o);
+  float* dw = dv + wave * MW * DH;                    // [MW][DH]
+  const int mw0 = m0 + MW * wave;
+#pragma unroll
+  for (int j = 0; j < MW; ++j) {
+    const int m = min(mw0 + j, a.M - 1);
+    for (int c = lane; c < DH; c += 64) dw[j * DH + c] = ob[c] - a.means_v[(long long)m * a.D + h * DH + c];
+  }
+  __syncthreads();
+  float y1[MW], y2[MW];
+#pragma unroll
+  for (int j = 0; j < MW; ++j) { y1[j] = 0.0f; y2[j] = 0.0f; }
+  const int l1 = lane < DH ? lane : 0;
+#pragma unroll 4
+  for (int c = 0; c < DH; ++c) {
+    const float g1 = G[c * DH + l1];
+    const float g2 = DH > 64 ? G[c * DH + lane + 64] : 0.0f;
+#pragma unroll
+    for (int j = 0; j < MW; ++j) {
+      const float dc = dw[j * DH + c];
+      y1[j] = fmaf(g1, dc, y1[j]);
+      if (DH > 64) y2[j] = fmaf(g2, dc, y2[j]);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < MW; ++j) {
+    const int m = mw0 + j;
+    float part = lane < DH ? dw[j * DH + lane] * y1[j] : 0.0f;
+    if (DH > 64) part += dw[j * DH + lane + 64] * y2[j];
+    for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o);
+    if (m < a.M && lane == 0) {
       const float pi = e[m] / ssum;
       const float cf = pi / (1.0f - pi + a.eps);
       const float u = cf * cf * part;
-      if (lane == 0) {
-        const long long o = ((long long)i * a.H + h) * a.M + m;
-        a.u[o] = u;
-        if (a.u_out) a.u_out[o] = u;
-      }
+      const long long o = ((long long)i * a.H + h) * a.M + m;
+      a.u[o] = u;
+      if (a.u_out) a.u_out[o] = u;
     }
-    __syncthreads();
   }
 }
 
 // ---------------------------------------------------------------------------
 // Algorithm 1 (eq:gain, eq:boundarygain, eq:topk)
 // ---------------------------------------------------------------------------
-// In-LDS bitonic sort of P (power of two) 64-bit keys into descending order.
-__device__ void bitonic_desc(unsigned long long* key, int P) {
+// In-LDS bitonic sort of P (power of two) 64-bit keys into descending order by
+// the nthr threads of the workgroup.
+__device__ void bitonic_desc(unsigned long long* key, int P, int nthr) {
   for (int kk = 2; kk <= P; kk <<= 1) {
     for (int j = kk >> 1; j > 0; j >>= 1) {
-      for (int x = threadIdx.x; x < P; x += kThreads) {
+      for (int x = threadIdx.x; x < P; x += nthr) {
         const int y = x ^ j;
         if (y > x) {
           const unsigned long long p = key[x], q = key[y];
@@ -181,14 +203,15 @@ struct Coeffs {
   float al, bl, cl, ar, br, cr;
 };
 
-__global__ __launch_bounds__(kThreads) void coupled_refine_kernel(CoupledArgs a) {
+// One wave per head: the solver is a chain of small sorts and sums, and with a
+// single wave every barrier is immediate and every sum a shuffle butterfly.
+__global__ __launch_bounds__(kRefineThreads) void coupled_refine_kernel(CoupledArgs a) {
   extern __shared__ unsigned long long keys[];        // [P]
   const int M = a.M, n_a = a.n_a, k = a.k_eff, h = blockIdx.x;
   int P = 2;
   while (P < M) P <<= 1;
   float* g = reinterpret_cast<float*>(keys + P);      // [M] gains of the visited row
-  float* red = g + M;                                 // [kThreads]
-  uint32_t* xm = reinterpret_cast<uint32_t*>(red + kThreads);   // [n_a * M] retain bits
+  uint32_t* xm = reinterpret_cast<uint32_t*>(g + M);  // [n_a * M] retain bits
   __shared__ Coeffs cf;
   __shared__ float pair_ab[kCoupledMaxAnchors], pair_c[kCoupledMaxAnchors];
   const int tid = threadIdx.x;
@@ -200,7 +223,7 @@ __global__ __launch_bounds__(kThreads) void coupled_refine_kernel(CoupledArgs a)
   };
 
   // ---- coefficients
-  for (int j = tid; j + 1 < n_a; j += kThreads) {
+  for (int j = tid; j + 1 < n_a; j += kRefineThreads) {
     const float n = (float)(a.anchors[j + 1] - a.anchors[j]);
     pair_ab[j] = (n - 1.0f) * (2.0f * n - 1.0f) / (6.0f * n);
     pair_c[j] = (n * n - 1.0f) / (6.0f * n);
@@ -227,23 +250,23 @@ __global__ __launch_bounds__(kThreads) void coupled_refine_kernel(CoupledArgs a)
     }
     cf = c;
   }
-  for (int w = tid; w < nwords; w += kThreads) xm[w] = 0u;
+  for (int w = tid; w < nwords; w += kRefineThreads) xm[w] = 0u;
   __syncthreads();
 
   // TopK of the values in g[0..M): leaves the winners first in keys[], returns
   // their sum (the same on every thread)
   auto topk_sum = [&]() -> float {
-    for (int m = tid; m < P; m += kThreads) keys[m] = m < M ? order_key(g[m], m) : 0ull;
+    for (int m = tid; m < P; m += kRefineThreads) keys[m] = m < M ? order_key(g[m], m) : 0ull;
     __syncthreads();
-    bitonic_desc(keys, P);
+    bitonic_desc(keys, P, kRefineThreads);
     float s = 0.0f;
-    for (int x = tid; x < k; x += kThreads) s += g[~(uint32_t)(keys[x] & 0xffffffffull)];
-    return block_sum(s, red);
+    for (int x = tid; x < k; x += kRefineThreads) s += g[~(uint32_t)(keys[x] & 0xffffffffull)];
+    return wave_sum(s);
   };
   // row i's mask := the k winners left in keys[]
   auto apply_topk = [&](int i) {
     const int b0 = i * M, b1 = b0 + M;
-    for (int w = (b0 >> 5) + tid; w <= ((b1 - 1) >> 5); w += kThreads) {   // one owner per word
+    for (int w = (b0 >> 5) + tid; w <= ((b1 - 1) >> 5); w += kRefineThreads) {   // one owner per word
       uint32_t word = xm[w];
       for (int bb = 0; bb < 32; ++bb) {
         const int bit = (w << 5) + bb;
@@ -263,7 +286,7 @@ __global__ __launch_bounds__(kThreads) void coupled_refine_kernel(CoupledArgs a)
 
   // ---- initial masks: TopK(u) per anchor
   for (int i = 0; i < n_a; ++i) {
-    for (int m = tid; m < M; m += kThreads) g[m] = U(i, m);
+    for (int m = tid; m < M; m += kRefineThreads) g[m] = U(i, m);
     __syncthreads();
     topk_sum();
     apply_topk(i);
@@ -275,7 +298,7 @@ __global__ __launch_bounds__(kThreads) void coupled_refine_kernel(CoupledArgs a)
     return A * oa * ua + B * ob * ub + 2.0f * C * oa * ob * sqrtf(ua) * sqrtf(ub);
   };
   float jpart = 0.0f;
-  for (int m = tid; m < M; m += kThreads) {
+  for (int m = tid; m < M; m += kRefineThreads) {
     float anc = 0.0f, rec = 0.0f;
     for (int i = 0; i < n_a; ++i) anc += (1.0f - X(i, m)) * U(i, m);
     for (int j = 0; j + 1 < n_a; ++j) rec += risk(j, j + 1, pair_ab[j], pair_ab[j], pair_c[j], m);
@@ -283,7 +306,7 @@ __global__ __launch_bounds__(kThreads) void coupled_refine_kernel(CoupledArgs a)
     if (cf.has_r) rec += risk(n_a - 2, n_a - 1, cf.ar, cf.br, cf.cr, m);
     jpart += a.l_anc * anc + a.l_rec * rec;
   }
-  float J = block_sum(jpart, red);
+  float J = wave_sum(jpart);
 
   // ---- directional passes
   for (int s = 0; s < a.passes && k < M; ++s) {
@@ -291,7 +314,7 @@ __global__ __launch_bounds__(kThreads) void coupled_refine_kernel(CoupledArgs a)
     for (int v = 0; v < n_a; ++v) {
       const int i = (s % 2 == 0) ? v : n_a - 1 - v;
       float oldpart = 0.0f;
-      for (int m = tid; m < M; m += kThreads) {
+      for (int m = tid; m < M; m += kRefineThreads) {
         const float ui = U(i, m), si = sqrtf(ui);
         float G = a.l_anc * ui, rec = 0.0f;
         if (i > 0)
@@ -310,7 +333,7 @@ __global__ __launch_bounds__(kThreads) void coupled_refine_kernel(CoupledArgs a)
         g[m] = G;
         oldpart += X(i, m) * G;
       }
-      const float g_old = block_sum(oldpart, red);
+      const float g_old = wave_sum(oldpart);
       const float g_new = topk_sum();
       const float gain = g_new - g_old;
       if (gain > a.tol * fmaxf(J, 1e-8f)) {   // uniform: every thread holds the same sums
@@ -417,7 +440,7 @@ cast_status_t launch_coupled(const void* q, const void* k, const void* v, const 
   st = launch_pool_means(v, v, 0, S, M, Bv, p.v, partial, const_cast<float*>(a.means_v), stream);
   if (st != CAST_OK) return st;
   const dim3 grid(n_a * H, (M + kOmM - 1) / kOmM);
-  const size_t shm = (size_t)(M + 2 * dh + kThreads + 4 * dh) * sizeof(float);
+  const size_t shm = (size_t)(M + 2 * dh + kThreads + kOmM * dh) * sizeof(float);
   switch (dh) {
     case 32: hipLaunchKernelGGL(coupled_omission_kernel<32>, grid, dim3(kThreads), shm, stream, a); break;
     case 64: hipLaunchKernelGGL(coupled_omission_kernel<64>, grid, dim3(kThreads), shm, stream, a); break;
@@ -427,8 +450,8 @@ cast_status_t launch_coupled(const void* q, const void* k, const void* v, const 
   if (st != CAST_OK) return st;
   int P = 2;
   while (P < M) P <<= 1;
-  const size_t shm2 = (size_t)P * 8 + (size_t)M * 4 + kThreads * 4 + (size_t)((n_a * M + 31) / 32) * 4;
-  hipLaunchKernelGGL(coupled_refine_kernel, dim3(H), dim3(kThreads), shm2, stream, a);
+  const size_t shm2 = (size_t)P * 8 + (size_t)M * 4 + (size_t)((n_a * M + 31) / 32) * 4;
+  hipLaunchKernelGGL(coupled_refine_kernel, dim3(H), dim3(kRefineThreads), shm2, stream, a);
   return check_launch("coupled_refine");
 }
 
