@@ -26,6 +26,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 COPY_BYTES = 1 << 29          # 512 MiB fp32 copy: larger than the Infinity Cache
+COPY_KERNEL = "__amd_rocclr_copyBuffer"   # the HIP runtime's device-to-device copy
+CALIB_REPS = 3
 KERNEL_SOURCES = {
     "route": ["route_kv.hip"],
     "attn": ["anchor_attn.hip"],
@@ -51,7 +53,7 @@ def part_of(kernel: str) -> str | None:
     return None
 
 
-def run(workload: str, reps: int = 3) -> None:
+def run(workload: str, reps: int = CALIB_REPS) -> None:
     if ROOT not in sys.path:
         sys.path.insert(0, ROOT)
     import torch
@@ -98,20 +100,34 @@ def _short(n: str) -> str:
         "cast::pardev::", "")
 
 
+def _calibration(db: str, counter: str, reps: int = CALIB_REPS) -> float:
+    """Mean reading of the calibration copies: the first `reps` dispatches of the
+    runtime's device-to-device copy kernel (run() issues them before anything else;
+    other kernels with "copy" in their name, such as dtype conversions, are not it)."""
+    con = sqlite3.connect(db)
+    rows = con.execute("select dispatch_id, counter_value from pmc_events where name = ? and "
+                       "counter_name = ? order by dispatch_id", (COPY_KERNEL, counter)).fetchall()
+    if len(rows) < reps:
+        raise SystemExit(f"{db}: expected {reps} calibration copies ({COPY_KERNEL}), "
+                         f"found {len(rows)}")
+    vals = [v for _, v in rows[:reps]]
+    if max(vals) > 1.01 * min(vals):
+        raise SystemExit(f"{db}: calibration copies disagree: {vals}")
+    return sum(vals) / len(vals)
+
+
 def summarize(workload: str, fetch_db: str, write_db: str, cmd: str, out_stem: str) -> None:
     fetch = _per_kernel(fetch_db, "FETCH_SIZE")
     write = _per_kernel(write_db, "WRITE_SIZE")
-    copy_f = [v for n, (v, _) in fetch.items() if "copy" in n.lower()]
-    copy_w = [v for n, (v, _) in write.items() if "copy" in n.lower()]
-    if not copy_f or not copy_w:
-        raise SystemExit("no copy kernel found in the counter databases")
     kib = COPY_BYTES / 1024.0
-    f_scale = kib / max(copy_f)      # bytes-per-KiB-reading scale: 1.0 when the counter is exact
-    w_scale = kib / max(copy_w)
+    copy_f = _calibration(fetch_db, "FETCH_SIZE")
+    copy_w = _calibration(write_db, "WRITE_SIZE")
+    f_scale = kib / copy_f           # bytes-per-KiB-reading scale: 1.0 when the counter is exact
+    w_scale = kib / copy_w
     kernels = {}
     for n in sorted(set(fetch) | set(write)):
         part = part_of(n)
-        if part is None:
+        if part is None or n == COPY_KERNEL:
             continue
         fb = fetch.get(n, (0.0, 0))[0] * f_scale * 1024.0
         wb = write.get(n, (0.0, 0))[0] * w_scale * 1024.0
@@ -123,7 +139,7 @@ def summarize(workload: str, fetch_db: str, write_db: str, cmd: str, out_stem: s
         for key in ("fetch_bytes", "write_bytes", "bytes"):
             p[key] += v[key]
     doc = {"workload": workload, "copy_bytes": COPY_BYTES,
-           "copy_counter_kib": {"FETCH_SIZE": max(copy_f), "WRITE_SIZE": max(copy_w)},
+           "copy_counter_kib": {"FETCH_SIZE": copy_f, "WRITE_SIZE": copy_w},
            "scale": {"FETCH_SIZE": f_scale, "WRITE_SIZE": w_scale},
            "sources": {p: sources_hash(p) for p in KERNEL_SOURCES},
            "kernels": kernels, "per_call_bytes": parts, "command": cmd}

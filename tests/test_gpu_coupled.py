@@ -21,8 +21,8 @@ from test_gpu_parity import log, np64
 
 pytestmark = pytest.mark.gpu
 
-U_REL_RMS = 1e-3
-MARGIN = 1e-4      # >= 100x the float32 error of u (rel-RMS ~1e-7)
+U_REL_RMS = 1e-4  # float32 token means over up to 3520 tokens: measured rel-RMS <= 3.4e-6
+MARGIN = 1e-4     # decision margin that the float32 search must resolve like float64
 
 
 def oracle_means(q, k, v):
