@@ -93,9 +93,7 @@ __device__ __forceinline__ int xcd_remap(int b, int nb) {
 
 // v_max3_f32 (the compiler forms it only from some max chains)
 __device__ __forceinline__ float max3f(float x, float y, float z) {
-  float r;
-  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(y), "v"(z));
-  return r;
+  return __builtin_fmaxf(__builtin_fmaxf(x, y), z);
 }
 
 // Row sums add the bf16 probabilities that enter P V, two per v_dot2 with (1, 1).
@@ -146,14 +144,18 @@ __device__ __forceinline__ constexpr int vswz(int r, int cpr) {
   return ((2 * (r & 3)) ^ (8 * (r & 1))) & (cpr - 1);
 }
 
-// FAST: no current segment and chunks of >= 64 rows, so every tile takes the
-// uniform two-chunk mapping and its copies can be issued inside the MFMA block.
+// MODE 1 (fast): no current segment and chunks of >= 64 rows, so every tile takes
+// the uniform two-chunk mapping and its copies can be issued inside the MFMA
+// block.  MODE 2 (aligned): also chunks of a multiple of 64 rows, so no tile
+// crosses a chunk and each copy is one uniform base plus the lane's fixed offset.
+// MODE 0: the general path (current segment, short chunks).
 // Each wave owns QB = 2 blocks of 32 queries: every K / V operand read from LDS
 // feeds two MFMAs, which halves the LDS read traffic per MFMA (with one block
 // per wave the LDS port, not the matrix core, is the limit).  The O accumulators
 // live in the AGPR file; one workgroup runs per CU.
-template <int DH, bool FAST>
+template <int DH, int MODE>
 __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
+  constexpr bool FAST = MODE >= 1, ALIGNED = MODE == 2;
   constexpr int QB = 2;
   using G = Geo<DH>;
   constexpr int BQ = kBQ;
@@ -219,14 +221,14 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
     const int r = slot_row(n), pc = lane % G::CPR;
     return (unsigned)((pc ^ (is_v ? vswz(r, G::CPR) : kswz(r, G::CPR))) * 16);
   };
-  auto copy16 = [&](__amdgpu_buffer_rsrc_t rs, uint16_t* dst, int n, unsigned off)
+  auto copy16 = [&](__amdgpu_buffer_rsrc_t rs, uint16_t* dst, int n, unsigned off, unsigned soff)
       __attribute__((always_inline)) {
     // recomputed at each use (the laundering stops the compiler from keeping the
     // LDS bases of all buffers live in scalar registers across the loop)
     int wbase = wave * G::DPT * 1024;
     asm volatile("" : "+s"(wbase));
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
-        rs, (lds_void*)(reinterpret_cast<char*>(dst) + wbase + n * 1024), 16, (int)off, 0, 0, 0);
+        rs, (lds_void*)(reinterpret_cast<char*>(dst) + wbase + n * 1024), 16, (int)off, (int)soff, 0, 0);
   };
   // Row j of tile `tile` is sequence row r = 64*tile + j: current segment rows
   // r < n0, then routed chunk rows.  History-only tiles with chunks of >= 64 rows
@@ -249,8 +251,13 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
   auto copy_fast = [&](auto is_v, const TileMap& m, int n, uint16_t* dst) __attribute__((always_inline)) {
     constexpr bool IsV = decltype(is_v)::value != 0;
     const int r = slot_row(n);
-    const unsigned off = (r < m.split ? m.base0 : m.base1) + (unsigned)r * row_bytes + slot_off(n, IsV);
-    copy16(tensor_rsrc(IsV ? a.v : a.k, a.hist_bytes), dst, n, off);
+    const unsigned lane_off = (unsigned)r * row_bytes + slot_off(n, IsV);
+    if constexpr (ALIGNED) {
+      copy16(tensor_rsrc(IsV ? a.v : a.k, a.hist_bytes), dst, n, lane_off, m.base0);
+    } else {
+      copy16(tensor_rsrc(IsV ? a.v : a.k, a.hist_bytes), dst, n,
+             (r < m.split ? m.base0 : m.base1) + lane_off, 0u);
+    }
   };
   // Copy tile `tile` of K (is_v = 0) or V (is_v = 1) into `dst`.
   auto load_tile = [&](auto is_v, int tile, uint16_t* dst) __attribute__((always_inline)) {
@@ -276,8 +283,8 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
         // merged into one copy with a per-lane descriptor)
         if (r < a.n0)
           copy16(tensor_rsrc(IsV ? a.vc : a.kc, a.cur_bytes), dst, n,
-                 (unsigned)r * row_bytes + head_bytes + co);
-        if (r >= a.n0) copy16(rh, dst, n, hoff);
+                 (unsigned)r * row_bytes + head_bytes + co, 0u);
+        if (r >= a.n0) copy16(rh, dst, n, hoff, 0u);
       }
     }
   };
@@ -369,17 +376,12 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
   //   IsPV = 1: O^T[qb] += V^T P^T[qb] from the V tile `src` with operands `pp`.
   auto phase = [&](auto is_pv, auto do_mm, auto do_sm, auto do_copy, const uint16_t* src, SAcc& sn,
                    const PAcc& pp, SBlk& ss, PBlk& ps, float& corr, bool& up, int qbs, uint16_t* kdst,
-                   int tk, uint16_t* vdst, int tv) __attribute__((always_inline)) {
+                   const TileMap& mk, uint16_t* vdst, const TileMap& mv) __attribute__((always_inline)) {
     constexpr bool IsPV = decltype(is_pv)::value != 0, MM = decltype(do_mm)::value != 0;
     constexpr bool SM = decltype(do_sm)::value != 0;
     constexpr bool COPY = decltype(do_copy)::value != 0;
     constexpr int NSL = (MM ? NM : 0) > 32 ? NM : 32;
     constexpr int kLA = 2;
-    TileMap mk{}, mv{};
-    if constexpr (COPY) {
-      mk = tile_map(tk);
-      mv = tile_map(tv);
-    }
     bf16x8 op[NR];
     float pm = 0.0f, m_new = 0.0f, rs = 0.0f;
     float pe[32];
@@ -479,6 +481,41 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
   // Iteration 0 meets tile -1 (all -inf, P = 0, V buffer zeroed); iteration nt
   // computes a throw-away S from a stale K tile whose block-0 softmax is fully
   // masked.  Every iteration runs the same straight-line phases.
+  // Copy cursors of the fast path: the tile being copied sits at row `off` of
+  // routed slot `s` (chunks c0 = sidx[s], c1 = sidx[s + 1]); advancing by one tile
+  // crosses at most one chunk boundary (chunks have >= 64 rows), so no division.
+  struct Cursor { int s, off, c0, c1; };
+  auto cursor_at = [&](int tile) __attribute__((always_inline)) -> Cursor {
+    Cursor c;
+    const int u0 = tile * kBK;
+    c.s = u0 / a.Bv;
+    c.off = u0 - c.s * a.Bv;
+    c.c0 = __builtin_amdgcn_readfirstlane(sidx[c.s]);
+    c.c1 = __builtin_amdgcn_readfirstlane(sidx[c.s + 1]);
+    return c;
+  };
+  auto advance = [&](Cursor& c) __attribute__((always_inline)) {
+    c.off += kBK;
+    if (c.off >= a.Bv) {
+      c.off -= a.Bv;
+      c.s += 1;
+      c.c0 = c.c1;
+      c.c1 = __builtin_amdgcn_readfirstlane(sidx[c.s + 1]);
+    }
+  };
+  auto cur_map = [&](const Cursor& c) __attribute__((always_inline)) -> TileMap {
+    TileMap m;
+    m.base0 = (unsigned)(c.c0 * a.Bv + c.off) * row_bytes + head_bytes;
+    m.base1 = (unsigned)(c.c1 * a.Bv + c.off - a.Bv) * row_bytes + head_bytes;
+    m.split = a.Bv - c.off;
+    return m;
+  };
+  Cursor cur_k{}, cur_v{};
+  if constexpr (FAST) {
+    cur_k = cursor_at(min(1, nt - 1));
+    cur_v = cursor_at(0);
+  }
+
   auto step = [&](auto par, int j, SAcc& sc, SAcc& sp, PAcc& pc, PAcc& pp, float& c0c, bool& u0c,
                   float& c0p, bool& u0p, float& c1p, bool& u1p) __attribute__((always_inline)) {
     constexpr int B = decltype(par)::value;
@@ -494,8 +531,17 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
       load_tile(IC<1>{}, tv, vcur);
     }
     if (j == nt) mask_tile(sp[1], j - 1);
+    TileMap mk{}, mv{};
+    if constexpr (FAST) {
+      mk = cur_map(cur_k);
+      mv = cur_map(cur_v);
+    }
     phase(IC<0>{}, IC<1>{}, IC<1>{}, IC<FAST ? 1 : 0>{}, kcur, sc, pp, sp[1], pp[1], c1p, u1p, 1,
-          knext, tk, vcur, tv);
+          knext, mk, vcur, mv);
+    if constexpr (FAST) {
+      if (j + 2 < nt) advance(cur_k);
+      if (j + 1 < nt) advance(cur_v);
+    }
     // O rescale before O += P[j-1] V[j-1]: block 0 by tile j-1's factor (phase 2 of
     // the previous iteration), block 1 by the one just computed
     if (__ballot(u0p || u1p) != 0ull) {
@@ -507,8 +553,8 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
       });
     }
     if (j >= nt - 1) mask_tile(sc[0], j);
-    phase(IC<1>{}, IC<1>{}, IC<1>{}, IC<0>{}, vprev, sc, pp, sc[0], pc[0], c0c, u0c, 0, nullptr, 0,
-          nullptr, 0);
+    phase(IC<1>{}, IC<1>{}, IC<1>{}, IC<0>{}, vprev, sc, pp, sc[0], pc[0], c0c, u0c, 0, nullptr, mk,
+          nullptr, mv);
   };
 
   // zero the V buffer that iteration 0 reads as V[-1] (P[-1] = 0 must not meet NaN)
@@ -550,10 +596,12 @@ template <int DH>
 cast_status_t launch_dh(AttnArgs a, hipStream_t stream) {
   a.n_qt = (a.S + kBQ - 1) / kBQ;
   a.nblocks = a.n_a * a.H * a.n_qt;
-  if (a.n0 == 0 && a.Bv >= kBK)
-    hipLaunchKernelGGL((anchor_attn_kernel<DH, true>), dim3(a.nblocks), dim3(kThreads), 0, stream, a);
+  if (a.n0 == 0 && a.Bv % kBK == 0)
+    hipLaunchKernelGGL((anchor_attn_kernel<DH, 2>), dim3(a.nblocks), dim3(kThreads), 0, stream, a);
+  else if (a.n0 == 0 && a.Bv >= kBK)
+    hipLaunchKernelGGL((anchor_attn_kernel<DH, 1>), dim3(a.nblocks), dim3(kThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL((anchor_attn_kernel<DH, false>), dim3(a.nblocks), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL((anchor_attn_kernel<DH, 0>), dim3(a.nblocks), dim3(kThreads), 0, stream, a);
   return check_launch("anchor_attn");
 }
 
