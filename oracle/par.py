@@ -68,6 +68,7 @@ class ParParams:
     eps: float = EPS
     gate_mode: int = GATE_PAR   # 0: eq:gate, 1: g == 1 (full transport), 2: g == 0 (linear)
     accumulate: bool = False    # False: out[t] = R_hat_t ; True: out[t] += R_hat_t (eq:block)
+    update_anchors: bool = False  # also the anchor case of eq:block: out[a] (+)= R_a
 
 # ----------------------------------------------------------------------------
 # Tiles and the 2-D real DFT (App. A.2: disjoint tiles, orthonormal, own size)
@@ -308,12 +309,21 @@ def reconstruct_frame(stats_for_pair, alpha: float, Hg: int, Wg: int, D: int) ->
         out[y0:y0 + hp, x0:x0 + wp, :] = irfft2_ortho(Fh, wp)
     return out
 
+def anchor_update(out: np.ndarray, resid: np.ndarray, anchors, accumulate: bool) -> None:
+    """The anchor case of eq:block: an anchor's update is its own directly
+    computed residual, R~_a = R_a (in place on `out`)."""
+    for a in anchors:
+        r = np.asarray(resid[a], dtype=np.float64)
+        out[a] = out[a] + r if accumulate else r
+
 def par_reconstruct(resid: np.ndarray, anchors, prm: ParParams = ParParams(),
                     out: np.ndarray | None = None, targets=None) -> np.ndarray:
     """Apply PAR to every skipped frame (or to the listed `targets` only).
 
     Write mode: out[t] = R_hat_t.  Accumulate mode: out[t] += R_hat_t.
-    Anchor slots of `out` are never touched.  Returns `out` (float64).
+    Anchor slots of `out` are touched only with `update_anchors`, which applies
+    the anchor case of eq:block as well (out[a] = R_a, or out[a] += R_a).
+    Returns `out` (float64).
     """
     n_frames, Hg, Wg, D = resid.shape
     comp = composition(anchors, n_frames)
@@ -321,6 +331,8 @@ def par_reconstruct(resid: np.ndarray, anchors, prm: ParParams = ParParams(),
         out = np.zeros(resid.shape, dtype=np.float64)
     else:
         out = np.array(out, dtype=np.float64, copy=True)
+    if prm.update_anchors:
+        anchor_update(out, resid, anchors, prm.accumulate)
     if not comp:
         return out
     stats = par_stats(resid, anchors, prm)
@@ -333,6 +345,16 @@ def par_reconstruct(resid: np.ndarray, anchors, prm: ParParams = ParParams(),
         else:
             out[t] = r
     return out
+
+def block_sites(x: np.ndarray, site_residuals, anchors, prm: ParParams = ParParams()) -> np.ndarray:
+    """One transformer block's eligible residual sites (visual attention, then
+    FFN) sharing one anchor set (Sec. 4.1): each site's update is added to the
+    current-frame hidden state per eq:block, anchors included.  `site_residuals`
+    are the residual buffers of the sites in order (only anchor frames read)."""
+    p = ParParams(**{**prm.__dict__, "accumulate": True, "update_anchors": True})
+    for r in site_residuals:
+        x = par_reconstruct(r, anchors, p, out=x)
+    return x
 
 def par_reconstruct_targets(resid: np.ndarray, anchors, targets, prm: ParParams = ParParams()):
     """R_hat_t for the listed skipped frames only, as {t: [Hg, Wg, D] float64}.

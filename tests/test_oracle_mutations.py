@@ -95,6 +95,21 @@ def _composition_wrong_pair(anchors, n):
     return out
 
 
+def _anchor_update_twice(out, resid, anchors, accumulate):
+    for a in anchors:
+        out[a] = out[a] + 2.0 * resid[a] if accumulate else resid[a]
+
+
+def _anchor_update_skip_last(out, resid, anchors, accumulate):
+    for a in list(anchors)[:-1]:
+        out[a] = out[a] + resid[a] if accumulate else resid[a]
+
+
+def _anchor_update_always_adds(out, resid, anchors, accumulate):
+    for a in anchors:
+        out[a] = out[a] + resid[a]
+
+
 PAR_MUTANTS = {
     "cross_no_conj": dict(cross_spectrum=_cross_no_conj),
     "cross_swapped": dict(cross_spectrum=_cross_swapped),
@@ -105,6 +120,9 @@ PAR_MUTANTS = {
     "wrap_no_canon": dict(wrap_arg=_wrap_no_canon),
     "kappa_all_one": dict(bin_tables=_bin_tables_kappa1),
     "mirror_rep_swapped": dict(bin_tables=_bin_tables_mirror_swap),
+    "anchor_update_twice": dict(anchor_update=_anchor_update_twice),
+    "anchor_update_skip_last": dict(anchor_update=_anchor_update_skip_last),
+    "anchor_update_always_adds": dict(anchor_update=_anchor_update_always_adds),
 }
 
 

@@ -305,11 +305,57 @@ def pin_wrap(mod=P):
     assert abs(mod.wrap_arg(-1j) + math.pi / 2) < 1e-15
 
 
+def pin_anchor_update(mod=P):
+    """eq:block, anchor case: an anchor's update is its own residual.  With
+    update_anchors every anchor slot becomes x0 + R_a (accumulate) or R_a
+    (write) exactly, and every skipped slot is what it is without the option;
+    with K_f = N_cur every frame is an anchor."""
+    n, hg, wg, d = 7, 8, 8, 3
+    r = rng(41).standard_normal((n, hg, wg, d))
+    x0 = rng(42).standard_normal((n, hg, wg, d))
+    anchors = [1, 3, 6]
+    base = mod.par_reconstruct(r, anchors, mod.ParParams(accumulate=True), out=x0)
+    upd = mod.par_reconstruct(r, anchors, mod.ParParams(accumulate=True, update_anchors=True), out=x0)
+    wr = mod.par_reconstruct(r, anchors, mod.ParParams(update_anchors=True), out=x0)
+    for t in range(n):
+        if t in anchors:
+            assert np.array_equal(upd[t], x0[t] + r[t])
+            assert np.array_equal(wr[t], r[t])
+            assert np.array_equal(base[t], x0[t])
+        else:
+            assert np.array_equal(upd[t], base[t])
+    allf = mod.par_reconstruct(r, list(range(n)),
+                               mod.ParParams(accumulate=True, update_anchors=True), out=x0)
+    assert np.array_equal(allf, x0 + r)
+
+
+def pin_sites_linear_g0(mod=P):
+    """With g = 0 each site's reconstruction is linear in its residual
+    (eq:fcpasm), so an attention site and an FFN site sharing the anchors add up
+    to one site with the summed residuals, anchors included; a skipped frame then
+    gets (1 - alpha) R_a + alpha R_b summed over the sites."""
+    n, hg, wg, d = 6, 8, 6, 3
+    r1 = rng(51).standard_normal((n, hg, wg, d))
+    r2 = rng(52).standard_normal((n, hg, wg, d))
+    x0 = rng(53).standard_normal((n, hg, wg, d))
+    anchors = [1, 4]
+    prm = mod.ParParams(gate_mode=mod.GATE_ZERO)
+    two = mod.block_sites(x0, [r1, r2], anchors, prm)
+    one = mod.block_sites(x0, [r1 + r2], anchors, prm)
+    assert np.allclose(two, one, rtol=0, atol=1e-12)
+    s = r1 + r2
+    for t, alpha in ((2, 1 / 3), (0, -1 / 3), (5, 4 / 3)):
+        want = x0[t] + (1 - alpha) * s[1] + alpha * s[4]
+        assert np.allclose(two[t], want, rtol=0, atol=1e-12), t
+    for a in anchors:
+        assert np.allclose(two[a], x0[a] + s[a], rtol=0, atol=1e-14)
+
+
 PINS = [pin_dft_bruteforce, pin_dft_numpy, pin_parseval_kappa, pin_round_trip, pin_bin_kinds,
         pin_nu_isotropy, pin_linear_g0, pin_translation_ramp, pin_endpoints, pin_real_valued,
         pin_confidence_bounds, pin_confidence_full_spectrum, pin_coherence_levels,
         pin_no_reliable_bin, pin_swap_symmetry, pin_channel_permutation, pin_gate_shape,
-        pin_wrap]
+        pin_wrap, pin_anchor_update, pin_sites_linear_g0]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
