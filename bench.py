@@ -55,6 +55,14 @@ def par_bytes(w, accumulate=True):
     return frame * (w.n_a + n_skip * (2 if accumulate else 1))
 
 
+def block_update_bytes(w):
+    """Algorithmic bytes of one residual site's whole block update (PAR with the
+    anchor case of eq:block fused in): anchors read once, then X read and written
+    for every current frame (fp32)."""
+    frame = 4.0 * w.S * w.D
+    return frame * (w.n_a + 2 * w.n_frames)
+
+
 def load_traffic(workload):
     """HBM bytes per call (route / attn / par) from the committed counter summary
     profiles/hbm_traffic_<workload>.json (written by paper_2609_34144_amd.hbm_traffic
@@ -264,6 +272,26 @@ def main():
         torch.cuda.synchronize()
         coupled_ms = float(np.mean([a.elapsed_time(b) for a, b in cm]))
 
+    # the whole update of one residual site (e.g. the FFN site): PAR of the skipped
+    # frames with every anchor's own update fused in, timed on its own
+    block_ms = None
+    if w.has_par:
+        bprm = cast.cast_par_params_default(accumulate=1, update_anchors=1)
+        bm = [[ev(), ev()] for _ in range(args.steps)]
+        for i in range(args.warmup):
+            s = sets[i % N_COPIES]
+            cast.cast_par_reconstruct(s["resid"], w.anchors, bprm, out=s["x"], workspace=par_ws,
+                                      stream=stream)
+        torch.cuda.synchronize()
+        for i in range(args.steps):
+            s = sets[i % N_COPIES]
+            bm[i][0].record(stream)
+            cast.cast_par_reconstruct(s["resid"], w.anchors, bprm, out=s["x"], workspace=par_ws,
+                                      stream=stream)
+            bm[i][1].record(stream)
+        torch.cuda.synchronize()
+        block_ms = float(np.mean([a.elapsed_time(b) for a, b in bm]))
+
     value = w.frame_tokens / (ms_step / 1e3)
     res = {
         "metric": "CAST block-step frame-tokens/s (routing + routed anchor attention + PAR)",
@@ -276,7 +304,7 @@ def main():
                    "history_chunks": w.M, "chunk_tokens": w.Bv, "topk": w.topk,
                    "par_mode": "accumulate", "input_copies": N_COPIES},
         "per_call_ms": {"route": route_ms, "attn": attn_ms, "par": par_ms,
-                        "route_coupled": coupled_ms},
+                        "route_coupled": coupled_ms, "par_block_update": block_ms},
     }
     extra = {}
     traffic = load_traffic(w.name)
@@ -301,6 +329,10 @@ def main():
         extra["par_hbm_gbps"] = pg
         extra["par_hbm_pct"] = 100.0 * pg / PEAK_HBM_GBS
         extra["par_traffic_bytes"] = traffic.get("par")
+        if block_ms:
+            bg = block_update_bytes(w) / (block_ms / 1e3) / 1e9
+            extra["par_block_update_hbm_gbps"] = bg
+            extra["par_block_update_hbm_pct"] = 100.0 * bg / PEAK_HBM_GBS
         if not w.has_attention:
             res["roofline"] = {"bound": "hbm", "kernel": "par (xspec+gate+recon)",
                                "achieved": pg, "peak": PEAK_HBM_GBS, "unit": "GB/s",

@@ -225,9 +225,17 @@ typedef struct {
                                   2: g = 0 (linear interpolation / extrapolation) */
   int accumulate;              /* 0: out[t] = R_hat_t;  1: out[t] += R_hat_t, i.e.
                                   X_t <- X_t + R~_t of eq:block */
+  int update_anchors;          /* 0: anchor slots of out are not touched;
+                                  1: also the anchor case of eq:block, R~_a = R_a:
+                                  out[a] = R_a (write) or out[a] += R_a (accumulate),
+                                  fused into the reconstruction pass; out must then
+                                  not overlap resid.  With accumulate = 1 one call
+                                  is the whole update of one eligible residual site
+                                  (visual attention or FFN) of a block. */
 } cast_par_params_t;
 
-/* Fill *p with the paper's settings (tab:config_cast, App. A.2), write mode. */
+/* Fill *p with the paper's settings (tab:config_cast, App. A.2), write mode,
+   anchor slots untouched. */
 void cast_par_params_default(cast_par_params_t* p);
 
 /* Device scratch (bytes) needed by cast_par_reconstruct for these sizes. */
@@ -253,8 +261,8 @@ size_t cast_par_workspace_bytes(int n_frames, int n_anchor, int Hg, int Wg, int 
  *
  * resid    fp32 [n_frames, Hg, Wg, D] device; only the anchor frames are read.
  * anchors  HOST int[n_anchor], strictly increasing in [0, n_frames); n_anchor >= 2
- *          unless n_anchor == n_frames (K_f = N_cur: nothing to reconstruct, no
- *          work enqueued, App. A.1).  n_frames <= 4096, n_anchor <= 512.
+ *          unless n_anchor == n_frames (K_f = N_cur: nothing to reconstruct, App.
+ *          A.1; no work is enqueued unless update_anchors is set).  n_frames <= 4096, n_anchor <= 512.
  * out      fp32 [n_frames, Hg, Wg, D] device; only skipped-frame slots are
  *          written (or accumulated into); anchor slots are never touched.  `out`
  *          may be `resid` itself (write mode fills the skipped slots in place).

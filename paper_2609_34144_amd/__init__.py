@@ -42,7 +42,7 @@ class ParParams(ctypes.Structure):
                 ("q", ctypes.c_float), ("T", ctypes.c_float),
                 ("eta_rel", ctypes.c_float), ("eta_abs", ctypes.c_float),
                 ("eps", ctypes.c_float), ("gate_mode", ctypes.c_int),
-                ("accumulate", ctypes.c_int)]
+                ("accumulate", ctypes.c_int), ("update_anchors", ctypes.c_int)]
 
 
 class CoupledParams(ctypes.Structure):

@@ -226,6 +226,7 @@ void cast_par_params_default(cast_par_params_t* p) {
   p->eps = 1e-8f;
   p->gate_mode = 0;
   p->accumulate = 0;
+  p->update_anchors = 0;
 }
 
 static cast_status_t par_shape_check(int n_frames, int n_anchor, int Hg, int Wg, int D,
@@ -239,6 +240,9 @@ static cast_status_t par_shape_check(int n_frames, int n_anchor, int Hg, int Wg,
   if (p->tile_h < 1 || p->tile_h > kParMaxTile || p->tile_w < 1 || p->tile_w > kParMaxTile)
     return fail(CAST_ERR_UNSUPPORTED, "par: tile edges must be in [1, %d]", kParMaxTile);
   if (p->gate_mode < 0 || p->gate_mode > 2) return fail(CAST_ERR_SHAPE, "par: gate_mode must be 0, 1 or 2");
+  if (p->accumulate != 0 && p->accumulate != 1) return fail(CAST_ERR_SHAPE, "par: accumulate must be 0 or 1");
+  if (p->update_anchors != 0 && p->update_anchors != 1)
+    return fail(CAST_ERR_SHAPE, "par: update_anchors must be 0 or 1");
   if (!(p->T > 0.0f) || !(p->q > 0.0f) || !(p->tau_high >= p->tau_low))
     return fail(CAST_ERR_SHAPE, "par: eq:gate needs q > 0, T > 0, tau_high >= tau_low");
   if ((long long)Hg * Wg * D >= (1LL << 30))
@@ -268,10 +272,20 @@ cast_status_t cast_par_reconstruct(const float* resid, const int* anchors, int n
     if (j > 0 && anchors[j] <= anchors[j - 1])
       return fail(CAST_ERR_ANCHORS, "par: anchors must be strictly increasing (index %d)", j);
   }
-  if (n_anchor == n_frames) return CAST_OK;                 // K_f = N_cur: bypass (App. A.1)
-  if (n_anchor < 2) return fail(CAST_ERR_ANCHORS, "par: reconstruction needs K_f >= 2 anchors");
+  const bool bypass = n_anchor == n_frames;                 // K_f = N_cur (App. A.1)
+  if (bypass && !params->update_anchors) return CAST_OK;
+  if (!bypass && n_anchor < 2) return fail(CAST_ERR_ANCHORS, "par: reconstruction needs K_f >= 2 anchors");
   if (resid == nullptr || out == nullptr) return fail(CAST_ERR_NULL, "par: resid and out are required");
   if (!aligned(resid, 4) || !aligned(out, 4)) return fail(CAST_ERR_SHAPE, "par: misaligned buffers");
+  if (params->update_anchors) {
+    // anchor slots of out are written while other blocks read the anchors of resid
+    const unsigned long long bytes = (unsigned long long)n_frames * Hg * Wg * D * sizeof(float);
+    const unsigned long long r0 = (unsigned long long)(uintptr_t)resid, o0 = (unsigned long long)(uintptr_t)out;
+    if (r0 < o0 + bytes && o0 < r0 + bytes)
+      return fail(CAST_ERR_SHAPE, "par: update_anchors needs out not to overlap resid");
+  }
+  if (bypass)
+    return launch_par_anchor_update(resid, anchors, n_anchor, Hg, Wg, D, params->accumulate, out, stream);
   ParPlan plan = plan_par(n_frames, n_anchor, Hg, Wg, D, *params);
   st = check_ws(workspace, workspace_bytes, plan.total);
   if (st != CAST_OK) return st;

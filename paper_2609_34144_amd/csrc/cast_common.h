@@ -104,5 +104,9 @@ cast_status_t launch_par(const float* resid, const int* anchors, int n_anchor, i
                          int Hg, int Wg, int D, const cast_par_params_t& p, float* out,
                          float* theta_out, float* gate_out, float* conf_out,
                          const ParPlan& plan, void* ws, hipStream_t stream);
+// K_f = N_cur with the anchor update: out[a] = R_a or out[a] += R_a for every frame
+cast_status_t launch_par_anchor_update(const float* resid, const int* anchors, int n_anchor,
+                                       int Hg, int Wg, int D, int accumulate, float* out,
+                                       hipStream_t stream);
 
 }  // namespace cast

@@ -229,6 +229,23 @@ int tile_classes(int Hg, int Wg, int th, int tw, ClassLaunch (&out)[4]) {
   return n;
 }
 
+// K_f = N_cur (every frame an anchor, nothing to reconstruct) with the anchor
+// update: out[a] = R_a or out[a] += R_a, four consecutive elements per thread.
+constexpr int kUpdThreads = 256;
+__global__ __launch_bounds__(kUpdThreads) void par_anchor_update_kernel(ParArgs a,
+                                                                        const float* __restrict__ resid,
+                                                                        float* __restrict__ out) {
+  const long long f = a.anchors[blockIdx.y];
+  const long long e0 = ((long long)blockIdx.x * kUpdThreads + threadIdx.x) * 4;
+  const float* src = resid + f * a.frame_elems;
+  float* dst = out + f * a.frame_elems;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const long long e = e0 + k;
+    if (e < a.frame_elems) dst[e] = a.accumulate ? dst[e] + src[e] : src[e];
+  }
+}
+
 }  // namespace
 
 ParPlan plan_par(int n_frames, int n_anchor, int Hg, int Wg, int D, const cast_par_params_t& p) {
@@ -279,6 +296,7 @@ cast_status_t launch_par(const float* resid, const int* anchors, int n_anchor, i
   a.eps = p.eps;
   a.gate_mode = p.gate_mode;
   a.accumulate = p.accumulate;
+  a.update_anchors = p.update_anchors;
   for (int j = 0; j < n_anchor; ++j) a.anchors[j] = (short)anchors[j];
 
   cast_status_t st;
@@ -332,6 +350,20 @@ cast_status_t launch_par(const float* resid, const int* anchors, int n_anchor, i
     if (st != CAST_OK) return st;
   }
   return CAST_OK;
+}
+
+cast_status_t launch_par_anchor_update(const float* resid, const int* anchors, int n_anchor,
+                                       int Hg, int Wg, int D, int accumulate, float* out,
+                                       hipStream_t stream) {
+  ParArgs a{};
+  a.frame_elems = (long long)Hg * Wg * D;
+  a.n_anchor = n_anchor;
+  a.accumulate = accumulate;
+  for (int j = 0; j < n_anchor; ++j) a.anchors[j] = (short)anchors[j];
+  const long long per_block = 4LL * kUpdThreads;
+  dim3 grid((unsigned)((a.frame_elems + per_block - 1) / per_block), (unsigned)n_anchor);
+  hipLaunchKernelGGL(par_anchor_update_kernel, grid, dim3(kUpdThreads), 0, stream, a, resid, out);
+  return check_launch("par_anchor_update");
 }
 
 }  // namespace cast

@@ -24,7 +24,7 @@ struct ParArgs {
   int tile_h, tile_w, n_tx, n_tiles;
   int n_anchor, n_chblk, bins_out;
   float tau_low, tau_high, q, T, eta_rel, eta_abs, eps;
-  int gate_mode, accumulate;
+  int gate_mode, accumulate, update_anchors;
   short anchors[kParMaxAnchors];
 };
 
@@ -209,6 +209,29 @@ constexpr int unique_slot(int ky, int kx) {
   return n + ky;
 }
 
+// The anchor case of eq:block on one (tile, channel): out[f] = R_f, or += R_f.
+template <int HP, int WP, bool ACC>
+__device__ __forceinline__ void anchor_tile_update(const ParArgs& a, const float* __restrict__ resid,
+                                                   float* __restrict__ out, int f, unsigned tile0,
+                                                   unsigned WgD4, unsigned D4, unsigned c4) {
+  const __amdgpu_buffer_rsrc_t src = frame_rsrc(resid, f, a.frame_elems);
+  const __amdgpu_buffer_rsrc_t dst = frame_rsrc(out, f, a.frame_elems);
+  fft::static_for<0, HP>([&](auto yy) {
+    constexpr int y = decltype(yy)::value;
+    float v[WP], o[WP];
+    fft::static_for<0, WP>([&](auto xx) {
+      constexpr int xi = decltype(xx)::value;
+      v[xi] = buf_ld(src, c4, tile0 + y * WgD4 + xi * D4);
+      if constexpr (ACC) o[xi] = buf_ld(dst, c4, tile0 + y * WgD4 + xi * D4);
+    });
+    fft::static_for<0, WP>([&](auto xx) {
+      constexpr int xi = decltype(xx)::value;
+      if constexpr (ACC) buf_st<0>(dst, c4, tile0 + y * WgD4 + xi * D4, o[xi] + v[xi]);
+      else buf_st<kNT>(dst, c4, tile0 + y * WgD4 + xi * D4, v[xi]);
+    });
+  });
+}
+
 template <int HP, int WP, bool ACC>
 __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __restrict__ resid,
                                            float* __restrict__ out,
@@ -223,6 +246,12 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
   const unsigned tile0 = 4u * (unsigned)((g.y0 * a.Wg + g.x0) * a.D);
   const unsigned WgD4 = 4u * (unsigned)(a.Wg * a.D), D4 = 4u * (unsigned)a.D;
   const int fa = a.anchors[pair], fb = a.anchors[pair + 1];
+  if (a.update_anchors) {
+    // pair p updates its left anchor, the last pair its right one too, so every
+    // anchor slot is written once (out does not overlap resid)
+    anchor_tile_update<HP, WP, ACC>(a, resid, out, fa, tile0, WgD4, D4, c4);
+    if (pair == a.n_anchor - 2) anchor_tile_update<HP, WP, ACC>(a, resid, out, fb, tile0, WgD4, D4, c4);
+  }
   float ar[HP][NKX], ai[HP][NKX];
   {
     // F_b is parked in this lane's LDS column (LDS as extra per-lane storage: no

@@ -72,7 +72,7 @@ def test_par_params_default_matches_paper(lib):
     assert abs(p.q - 2.0) < 1e-7 and abs(p.T - 0.10) < 1e-7
     assert abs(p.eta_rel - 1e-6) < 1e-12 and abs(p.eta_abs - 1e-8) < 1e-14
     assert abs(p.eps - 1e-8) < 1e-14
-    assert p.gate_mode == 0 and p.accumulate == 0
+    assert p.gate_mode == 0 and p.accumulate == 0 and p.update_anchors == 0
 
 
 def _route(lib, *, q=A, k=2 * A, n_a=2, S=64, H=2, dh=32, M=4, Bv=64, topk=2, idx=3 * A, keff=True,
@@ -148,6 +148,19 @@ def test_par_validation(lib):
     assert lib.cast_par_reconstruct(A, None, 2, 4, 8, 8, 64,
                                     ctypes.byref(cast.cast_par_params_default()), 2 * A, None,
                                     None, None, None, 0, None) == NULL
+
+
+def test_par_block_update_validation(lib):
+    """update_anchors writes anchor slots of out while anchors of resid are read:
+    out must not overlap resid; flags are 0 or 1; the bypass then needs buffers."""
+    assert _par(lib, [0, 3], update_anchors=2) == SHAPE
+    assert _par(lib, [0, 3], accumulate=2) == SHAPE
+    assert _par(lib, [0, 3], update_anchors=1, out=A) == SHAPE
+    assert _par(lib, [0, 3], update_anchors=1, out=A + 1024) == SHAPE
+    assert _par(lib, [0, 3], update_anchors=1, resid=2 * A, out=2 * A - 1024) == SHAPE
+    assert _par(lib, [0, 3], update_anchors=1) == WORKSPACE    # no overlap: reaches the workspace check
+    assert _par(lib, [0, 1, 2, 3], update_anchors=1, resid=None) == NULL
+    assert _par(lib, [0, 1, 2, 3], update_anchors=1, out=A + 4096) == SHAPE
 
 
 def test_par_bypass_all_anchors(lib):
