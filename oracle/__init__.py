@@ -14,9 +14,11 @@ par    Phase-Aware Reconstruction                     (Sec. 4.3 eq:cross .. eq:f
                                                        App. A.2, Sec. 4.1 eq:block)
 coupled  reconstruction-coupled historical routing    (Sec. 4.4 eq:omission .. eq:topk,
                                                        App. B, Algorithm 1)
+frame_select  control-aware frame selection         (Sec. 3.1 eq:sensitivity, Sec. 4.2
+                                                       eq:debt, eq:score, App. A.1)
 
 Every function computes in float64 on the values it is given (bf16-rounded or
 fp32 inputs are widened first), written as the definition in the paper, with
 no blocking or fusion beyond what the definition states.
 """
-from . import route, attn, par, coupled  # noqa: F401
+from . import route, attn, par, coupled, frame_select  # noqa: F401

@@ -13,6 +13,8 @@ import oracle.route as R
 import oracle.attn as A
 import oracle.coupled as OC
 import test_oracle_coupled as TC
+import oracle.frame_select as FS
+import test_oracle_frame_select as TFS
 import test_oracle_par as TP
 import test_oracle_route_attn as TR
 
@@ -283,3 +285,58 @@ def test_coupled_refine_mutations_caught():
         mod = clone(OC, refine=ns["refine"])
         assert _any_pin_fails(mod, TC.PINS)
     del src
+
+
+# ---- control-aware frame selection
+F32 = np.float32
+
+
+def _fs_normalize_no_min(r, eps=1e-8):
+    r = np.asarray(r, dtype=F32)
+    return (r / (r.max() + F32(eps))).astype(F32)
+
+
+def _fs_sensitivity_always_half(rs, eps=1e-8):
+    got = [r for r in rs if r is not None]
+    if not got:
+        return None
+    acc = np.zeros(len(got[0]), dtype=F32)
+    for r in got:
+        acc = acc + FS.normalize(r, eps)
+    return (acc / F32(2)).astype(F32)
+
+
+def _fs_ages_no_reset(h, anchors, n_cur):
+    h = np.zeros(n_cur, dtype=np.int64) if h is None else np.asarray(h, dtype=np.int64)
+    return h + 1
+
+
+def _fs_debt_floor(h, n_cur, k_f):
+    return (np.asarray(h, dtype=F32) / F32(max(n_cur // k_f, 1))).astype(F32)
+
+
+def _fs_topk_high_index(s, k_f):
+    v = [float(x) for x in s]
+    order = sorted(range(len(v)), key=lambda i: (-v[i], -i))
+    return sorted(order[:k_f])
+
+
+def _fs_scores_no_lambda(d, debt, lambda_cov=0.5):
+    debt = np.asarray(debt, dtype=F32)
+    return debt if d is None else (np.asarray(d, dtype=F32) + debt).astype(F32)
+
+
+FS_MUTANTS = {
+    "normalize_no_min": dict(normalize=_fs_normalize_no_min),
+    "sensitivity_always_half": dict(sensitivity=_fs_sensitivity_always_half),
+    "ages_no_reset": dict(update_ages=_fs_ages_no_reset),
+    "debt_floor": dict(coverage_debt=_fs_debt_floor),
+    "topk_high_index": dict(topk_frames=_fs_topk_high_index),
+    "scores_no_lambda": dict(scores=_fs_scores_no_lambda),
+}
+
+
+@pytest.mark.parametrize("name", sorted(FS_MUTANTS))
+def test_frame_select_mutation_caught(name):
+    mod = clone(FS, **FS_MUTANTS[name])
+    assert _any_pin_fails(mod, TFS.PINS), f"no frame-selection pin catches mutation {name}"
