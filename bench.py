@@ -63,6 +63,12 @@ def block_update_bytes(w):
     return frame * (w.n_a + 2 * w.n_frames)
 
 
+def frame_select_bytes(w):
+    """Algorithmic bytes of frame selection: one read of both control branches'
+    bf16 updates of every current frame."""
+    return 2.0 * 2.0 * w.n_frames * w.S * w.D
+
+
 def load_traffic(workload):
     """HBM bytes per call (route / attn / par) from the committed counter summary
     profiles/hbm_traffic_<workload>.json (written by paper_2609_34144_amd.hbm_traffic
@@ -292,6 +298,31 @@ def main():
         torch.cuda.synchronize()
         block_ms = float(np.mean([a.elapsed_time(b) for a, b in bm]))
 
+    # control-aware frame selection for the next block (both control branches, bf16),
+    # timed on its own
+    sel_ms = None
+    if w.n_frames >= 2:
+        ctl = [gen.control_inputs(w, seed=args.seed + c, device=dev) for c in range(N_COPIES)]
+        ages = torch.zeros(w.n_frames, dtype=torch.int32, device=dev)
+        sel_out = torch.empty(len(w.anchors), dtype=torch.int32, device=dev)
+        nb = cast.cast_frame_select_workspace_bytes(w.n_frames, w.S, w.D)
+        sel_ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+        sm = [[ev(), ev()] for _ in range(args.steps)]
+        for i in range(args.warmup):
+            cam, act = ctl[i % N_COPIES]
+            cast.cast_frame_select(cam, act, w.anchors, len(w.anchors), ages, anchors_out=sel_out,
+                                   workspace=sel_ws, stream=stream)
+        torch.cuda.synchronize()
+        for i in range(args.steps):
+            cam, act = ctl[i % N_COPIES]
+            sm[i][0].record(stream)
+            cast.cast_frame_select(cam, act, w.anchors, len(w.anchors), ages, anchors_out=sel_out,
+                                   workspace=sel_ws, stream=stream)
+            sm[i][1].record(stream)
+        torch.cuda.synchronize()
+        sel_ms = float(np.mean([a.elapsed_time(b) for a, b in sm]))
+        del ctl
+
     value = w.frame_tokens / (ms_step / 1e3)
     res = {
         "metric": "CAST block-step frame-tokens/s (routing + routed anchor attention + PAR)",
@@ -304,7 +335,8 @@ def main():
                    "history_chunks": w.M, "chunk_tokens": w.Bv, "topk": w.topk,
                    "par_mode": "accumulate", "input_copies": N_COPIES},
         "per_call_ms": {"route": route_ms, "attn": attn_ms, "par": par_ms,
-                        "route_coupled": coupled_ms, "par_block_update": block_ms},
+                        "route_coupled": coupled_ms, "par_block_update": block_ms,
+                        "frame_select": sel_ms},
     }
     extra = {}
     traffic = load_traffic(w.name)
@@ -338,6 +370,10 @@ def main():
                                "achieved": pg, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                "frac": pg / PEAK_HBM_GBS, "traffic": traffic.get("par"),
                                "algorithmic_per_launch": par_bytes(w, True)}
+    if sel_ms:
+        fg = frame_select_bytes(w) / (sel_ms / 1e3) / 1e9
+        extra["frame_select_hbm_gbps"] = fg
+        extra["frame_select_hbm_pct"] = 100.0 * fg / PEAK_HBM_GBS
     res.update(extra)
     if not args.no_cpu_baseline:
         try:

@@ -6,5 +6,5 @@ paper's two backbones (Matrix-Game-like and HY-World-like blocks) and of two
 stress cases.  Both the HIP path and the oracle consume its outputs.
 """
 from .workloads import (  # noqa: F401
-    Workload, WORKLOADS, get, attn_inputs, par_inputs, seeds_for, wo_weight,
+    Workload, WORKLOADS, get, attn_inputs, par_inputs, seeds_for, wo_weight, control_inputs,
 )

@@ -178,6 +178,29 @@ def wo_weight(D: int, seed: int = 7, device="cpu"):
     return (_randn((D, D), seeds_for(seed, 1)[0], device) / float(np.sqrt(D))).to(torch.bfloat16)
 
 
+def control_inputs(w: Workload, seed: int = 42, device="cpu", n_cur=None, dtype=None):
+    """Feature updates of the camera and action control branches, [n_cur, S, D]
+    each (bf16 unless `dtype` is given), standing in for the trained branches'
+    outputs: N(0, 1) content times a per-frame magnitude.  The camera branch
+    peaks around one frame of the chunk (a control event), the action branch
+    varies frame to frame; both magnitudes lie in about [0.3, 3]."""
+    import torch
+    n = w.n_frames if n_cur is None else n_cur
+    s_cam, s_act, s_prof = seeds_for(seed, 3)
+    rng = np.random.default_rng(s_prof)
+    c = rng.uniform(0, n - 1)
+    t = np.arange(n)
+    mag_cam = 0.3 + 2.5 * np.exp(-((t - c) / 1.5) ** 2)
+    mag_act = rng.uniform(0.3, 3.0, size=n)
+    dt = torch.bfloat16 if dtype is None else dtype
+    out = []
+    for sd, mag in ((s_cam, mag_cam), (s_act, mag_act)):
+        x = _randn((n, w.S, w.D), sd, device)
+        x = x * torch.as_tensor(mag, dtype=torch.float32, device=x.device)[:, None, None]
+        out.append(x.to(dt))
+    return out[0], out[1]
+
+
 # ----------------------------------------------------------------------------
 # Residual fields (fp32)
 # ----------------------------------------------------------------------------

@@ -280,6 +280,60 @@ cast_status_t cast_par_reconstruct(const float* resid, const int* anchors, int n
                                    void* workspace, size_t workspace_bytes,
                                    hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Control-aware frame selection (Sec. 3.1 eq:sensitivity; Sec. 4.2 eq:debt,
+ * eq:score; App. A.1 eq:normalization and the scheduling rules)
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  float lambda_cov;   /* weight of the coverage debt: 0.5 (Sec. 4.2, tab:config_cast) */
+  float eps;          /* stabiliser of the min-max normalisation: 1e-8 */
+} cast_select_params_t;
+
+/* Fill *p with the paper's settings. */
+void cast_select_params_default(cast_select_params_t* p);
+
+/* Device scratch (bytes) needed by cast_frame_select (0 when no branch is given). */
+size_t cast_frame_select_workspace_bytes(int n_cur, int S, int D);
+
+/*
+ * Choose the anchors of the next transformer block after the current block ran
+ * with anchors_prev and its control branches produced the feature updates
+ * delta_cam and delta_act:
+ *   r_{i,k} = RMS of delta_k[i] over the frame's tokens and channels;
+ *   Norm_k = (r_k - min r_k) / (max r_k - min r_k + eps) over the N_cur frames;
+ *   d_i = mean of Norm_k over the branches given (an absent branch is left out);
+ *   ages: h_i = 0 for i in anchors_prev, h_i + 1 otherwise;
+ *   D_i = h_i / ceil(N_cur / K_f);  S_i = d_i + lambda_cov D_i, or lambda_cov D_i
+ *   when neither branch is given (no fresh control response);
+ *   anchors = the K_f largest S_i, ties by increasing frame index.
+ * Every step after r is fp32 with one rounding per operation (no contraction);
+ * r is the fp32 rounding of the square root of the mean of squares.
+ *
+ * delta_cam, delta_act  device [n_cur, S, D] of dtype (0: fp32, 1: bf16), frame-
+ *          major, channel-fastest; either or both may be NULL (absent branch).
+ * n_cur    current frames, 1 .. 4096;  S, D >= 1.
+ * anchors_prev  HOST int[n_prev], strictly increasing in [0, n_cur), n_prev >= 1:
+ *          the anchors the block ran with (all frames after a dense block, which
+ *          resets every age).
+ * k_f      anchors to choose, 1 .. n_cur.
+ * ages     device int32[n_cur], in/out: refresh ages before the block in, after
+ *          it out (start from zeros; the dense first block resets them anyway).
+ * r_out    device fp32[2, n_cur] or NULL: r per branch (row 0 camera, row 1
+ *          action; the row of an absent branch is not written).
+ * score_out  device fp32[n_cur] or NULL: S_i.
+ * anchors_out  device int32[k_f]: the chosen frames, ascending.
+ * workspace  device, 256-byte aligned, >= cast_frame_select_workspace_bytes.
+ * Errors: CAST_ERR_NULL (ages, anchors_out, params or anchors_prev missing),
+ * CAST_ERR_SHAPE (sizes, dtype, misaligned buffers, negative weights),
+ * CAST_ERR_ANCHORS (anchors_prev not strictly increasing in range),
+ * CAST_ERR_UNSUPPORTED (n_cur > 4096), CAST_ERR_WORKSPACE.
+ */
+cast_status_t cast_frame_select(const void* delta_cam, const void* delta_act, int dtype,
+                                int n_cur, int S, int D, const int* anchors_prev, int n_prev,
+                                int k_f, const cast_select_params_t* params, int32_t* ages,
+                                float* r_out, float* score_out, int32_t* anchors_out,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -25,7 +25,8 @@ EXPORTED = ["cast_status_string", "cast_last_error_detail", "cast_abi_version",
             "cast_route_kv_workspace_bytes", "cast_route_kv", "cast_anchor_attn",
             "cast_par_params_default", "cast_par_workspace_bytes", "cast_par_reconstruct",
             "cast_coupled_params_default", "cast_wo_gram", "cast_route_coupled_workspace_bytes",
-            "cast_route_coupled"]
+            "cast_route_coupled", "cast_select_params_default",
+            "cast_frame_select_workspace_bytes", "cast_frame_select"]
 
 
 class CastError(RuntimeError):
@@ -49,6 +50,11 @@ class CoupledParams(ctypes.Structure):
     """cast_coupled_params_t (include/cast.h)."""
     _fields_ = [("l_anc", ctypes.c_float), ("l_rec", ctypes.c_float),
                 ("passes", ctypes.c_int), ("tol", ctypes.c_float), ("eps", ctypes.c_float)]
+
+
+class SelectParams(ctypes.Structure):
+    """cast_select_params_t (include/cast.h)."""
+    _fields_ = [("lambda_cov", ctypes.c_float), ("eps", ctypes.c_float)]
 
 
 _lib = None
@@ -95,6 +101,13 @@ def load(path: str = LIB_PATH):
     lib.cast_route_coupled.argtypes = [_vp, _vp, _vp, _vp, _c.POINTER(_i), _i, _i, _i, _i, _i, _i,
                                        _i, _i, _f, _c.POINTER(CoupledParams), _vp, _vp,
                                        _c.POINTER(_i), _vp, _sz, _vp]
+    lib.cast_select_params_default.restype = None
+    lib.cast_select_params_default.argtypes = [_c.POINTER(SelectParams)]
+    lib.cast_frame_select_workspace_bytes.restype = _sz
+    lib.cast_frame_select_workspace_bytes.argtypes = [_i] * 3
+    lib.cast_frame_select.restype = _i
+    lib.cast_frame_select.argtypes = [_vp, _vp, _i, _i, _i, _i, _c.POINTER(_i), _i, _i,
+                                      _c.POINTER(SelectParams), _vp, _vp, _vp, _vp, _vp, _sz, _vp]
     _lib = lib
     return lib
 
@@ -219,6 +232,49 @@ def cast_route_coupled(q, k_hist, v_hist, gram, anchors, n_frames: int, topk: in
                                   _ptr(u_out), _ptr(idx_out), ctypes.byref(k_eff), _ptr(ws), wsb,
                                   _stream(stream)))
     return idx_out, k_eff.value, u_out
+
+
+def cast_select_params_default(**overrides) -> SelectParams:
+    p = SelectParams()
+    load().cast_select_params_default(ctypes.byref(p))
+    for k, v in overrides.items():
+        setattr(p, k, v)
+    return p
+
+
+def cast_frame_select_workspace_bytes(n_cur: int, S: int, D: int) -> int:
+    return load().cast_frame_select_workspace_bytes(n_cur, S, D)
+
+
+def cast_frame_select(delta_cam, delta_act, anchors_prev, k_f: int, ages,
+                      params: SelectParams | None = None, n_cur: int | None = None,
+                      r_out=None, score_out=None, anchors_out=None, workspace=None, stream=None):
+    """Control-aware frame selection.  delta_cam / delta_act: device [n_cur, S, D]
+    (fp32 or bf16, the same dtype) or None; `anchors_prev` the host anchors the
+    block ran with; `ages` device int32 [n_cur], updated in place.  Returns
+    anchors_out (device int32 [k_f], ascending)."""
+    import torch
+    lib = load()
+    if params is None:
+        params = cast_select_params_default()
+    given = [d for d in (delta_cam, delta_act) if d is not None]
+    if given:
+        n_cur, S, D = given[0].shape[0], given[0].shape[1], given[0].shape[2]
+        dtype = 0 if given[0].dtype == torch.float32 else 1
+        device = given[0].device
+    else:
+        n_cur, S, D, dtype, device = int(n_cur if n_cur is not None else ages.shape[0]), 1, 1, 0, ages.device
+    if anchors_out is None:
+        anchors_out = torch.empty(k_f, dtype=torch.int32, device=device)
+    anc = [int(a) for a in anchors_prev]
+    arr = (ctypes.c_int * max(len(anc), 1))(*anc)
+    nb = lib.cast_frame_select_workspace_bytes(n_cur, S, D) if given else 0
+    ws, wsb = _ws(nb, device, workspace)
+    _check(lib.cast_frame_select(_ptr(delta_cam), _ptr(delta_act), dtype, n_cur, S, D, arr,
+                                 len(anc), k_f, ctypes.byref(params), _ptr(ages), _ptr(r_out),
+                                 _ptr(score_out), _ptr(anchors_out), _ptr(ws), wsb,
+                                 _stream(stream)))
+    return anchors_out
 
 
 def cast_anchor_attn(q, k_hist, v_hist, idx, k_eff: int, scale: float, k_cur=None, v_cur=None,

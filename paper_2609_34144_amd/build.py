@@ -25,8 +25,6 @@ ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-Wall", "-Wno-unused-function", "-Wno-unused-variable"]
-# (source, object name, extra flags); par_fused.hip is compiled once per
-# bottom-remainder height of the 8x8 tiling (one row of the fused-kernel table)
 # (source, object name, extra flags), longest first; par_fused.hip is compiled
 # once per bottom-remainder height of the 8x8 tiling (one row of the
 # fused-kernel table)
@@ -39,6 +37,7 @@ UNITS = [("par.hip", "par", ["-fno-signed-zeros"])] + [
     ("anchor_attn.hip", "anchor_attn", ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]),
     ("route_kv.hip", "route_kv", []),
     ("route_coupled.hip", "route_coupled", []),
+    ("frame_select.hip", "frame_select", []),
     ("capi.hip", "capi", []),
 ]
 

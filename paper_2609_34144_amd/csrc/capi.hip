@@ -293,4 +293,59 @@ cast_status_t cast_par_reconstruct(const float* resid, const int* anchors, int n
                     gate_out, conf_out, plan, workspace, stream);
 }
 
+// ---------------------------------------------------------------------------
+// Control-aware frame selection
+// ---------------------------------------------------------------------------
+void cast_select_params_default(cast_select_params_t* p) {
+  if (p == nullptr) return;
+  p->lambda_cov = 0.5f;
+  p->eps = 1e-8f;
+}
+
+static cast_status_t select_shape_check(int n_cur, int S, int D) {
+  if (n_cur < 1 || S < 1 || D < 1) return fail(CAST_ERR_SHAPE, "frame_select: need n_cur, S, D >= 1");
+  if (n_cur > kSelectMaxFrames)
+    return fail(CAST_ERR_UNSUPPORTED, "frame_select: n_cur > %d", kSelectMaxFrames);
+  if ((long long)S * D >= (1LL << 40)) return fail(CAST_ERR_UNSUPPORTED, "frame_select: frame too large");
+  return CAST_OK;
+}
+
+size_t cast_frame_select_workspace_bytes(int n_cur, int S, int D) {
+  if (select_shape_check(n_cur, S, D) != CAST_OK) return 0;
+  return align_up((size_t)2 * n_cur * select_splits(S, D) * sizeof(float));
+}
+
+cast_status_t cast_frame_select(const void* delta_cam, const void* delta_act, int dtype,
+                                int n_cur, int S, int D, const int* anchors_prev, int n_prev,
+                                int k_f, const cast_select_params_t* params, int32_t* ages,
+                                float* r_out, float* score_out, int32_t* anchors_out,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (params == nullptr || anchors_prev == nullptr || ages == nullptr || anchors_out == nullptr)
+    return fail(CAST_ERR_NULL, "frame_select: params, anchors_prev, ages and anchors_out are required");
+  cast_status_t st = select_shape_check(n_cur, S, D);
+  if (st != CAST_OK) return st;
+  if (dtype != 0 && dtype != 1) return fail(CAST_ERR_SHAPE, "frame_select: dtype must be 0 (fp32) or 1 (bf16)");
+  if (!(params->lambda_cov >= 0.0f) || !(params->eps >= 0.0f) || params->lambda_cov > 1e30f || params->eps > 1e30f)
+    return fail(CAST_ERR_SHAPE, "frame_select: lambda_cov and eps must be finite and >= 0");
+  if (k_f < 1 || k_f > n_cur) return fail(CAST_ERR_SHAPE, "frame_select: k_f must be in [1, n_cur]");
+  if (n_prev < 1 || n_prev > n_cur) return fail(CAST_ERR_ANCHORS, "frame_select: n_prev must be in [1, n_cur]");
+  for (int j = 0; j < n_prev; ++j) {
+    if (anchors_prev[j] < 0 || anchors_prev[j] >= n_cur)
+      return fail(CAST_ERR_ANCHORS, "frame_select: anchor %d = %d outside [0, %d)", j, anchors_prev[j], n_cur);
+    if (j > 0 && anchors_prev[j] <= anchors_prev[j - 1])
+      return fail(CAST_ERR_ANCHORS, "frame_select: anchors must be strictly increasing (index %d)", j);
+  }
+  const size_t esz = dtype == 0 ? 4 : 2;
+  if (!aligned(ages, 4) || !aligned(anchors_out, 4) || !aligned(r_out, 4) || !aligned(score_out, 4) ||
+      !aligned(delta_cam, esz) || !aligned(delta_act, esz))
+    return fail(CAST_ERR_SHAPE, "frame_select: misaligned buffers");
+  if (delta_cam != nullptr || delta_act != nullptr) {
+    st = check_ws(workspace, workspace_bytes, cast_frame_select_workspace_bytes(n_cur, S, D));
+    if (st != CAST_OK) return st;
+  }
+  return launch_frame_select(delta_cam, delta_act, dtype, n_cur, S, D, anchors_prev, n_prev, k_f,
+                             *params, ages, r_out, score_out, anchors_out,
+                             static_cast<float*>(workspace), stream);
+}
+
 }  // extern "C"

@@ -109,4 +109,15 @@ cast_status_t launch_par_anchor_update(const float* resid, const int* anchors, i
                                        int Hg, int Wg, int D, int accumulate, float* out,
                                        hipStream_t stream);
 
+// ---------------------------------------------------------------------------
+// Control-aware frame selection
+// ---------------------------------------------------------------------------
+constexpr int kSelectMaxFrames = 4096;
+int select_splits(int S, int D);   // partial sums per (branch, frame)
+cast_status_t launch_frame_select(const void* cam, const void* act, int dtype, int n_cur, int S,
+                                  int D, const int* anchors_prev, int n_prev, int k_f,
+                                  const cast_select_params_t& p, int32_t* ages, float* r_out,
+                                  float* score_out, int32_t* anchors_out, float* partial,
+                                  hipStream_t stream);
+
 }  // namespace cast

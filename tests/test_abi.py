@@ -234,3 +234,40 @@ def test_wo_gram_validation(lib):
     assert lib.cast_wo_gram(A, 60, 2, 32, 2 * A, None) == SHAPE      # D != H * dh
     assert lib.cast_wo_gram(None, 64, 2, 32, 2 * A, None) == NULL
     assert lib.cast_wo_gram(A + 4, 64, 2, 32, 2 * A, None) == SHAPE
+
+
+# ---- control-aware frame selection
+def test_select_params_default_matches_paper(lib):
+    """Sec. 4.2 / tab:config_cast: lambda_cov = 0.5; stabiliser 1e-8 (reading)."""
+    p = cast.cast_select_params_default()
+    assert abs(p.lambda_cov - 0.5) < 1e-7 and abs(p.eps - 1e-8) < 1e-14
+
+
+def _fsel(lib, *, cam=A, act=2 * A, dtype=1, n_cur=4, S=64, D=64, prev=(0, 3), k_f=2,
+          params=None, ages=3 * A, r=None, sc=None, out=4 * A, ws=None, wsb=0, **pkw):
+    p = params if params is not None else cast.cast_select_params_default(**pkw)
+    arr = (ctypes.c_int * max(len(prev), 1))(*prev) if prev is not None else None
+    return lib.cast_frame_select(cam, act, dtype, n_cur, S, D, arr, len(prev or ()), k_f,
+                                 ctypes.byref(p), ages, r, sc, out, ws, wsb, None)
+
+
+def test_frame_select_validation(lib):
+    assert _fsel(lib, ages=None) == NULL
+    assert _fsel(lib, out=None) == NULL
+    assert _fsel(lib, prev=None) == NULL
+    assert _fsel(lib, dtype=2) == SHAPE
+    assert _fsel(lib, k_f=0) == SHAPE
+    assert _fsel(lib, k_f=5) == SHAPE
+    assert _fsel(lib, S=0) == SHAPE
+    assert _fsel(lib, lambda_cov=-1.0) == SHAPE
+    assert _fsel(lib, prev=(3, 0)) == ANCHORS
+    assert _fsel(lib, prev=(0, 4)) == ANCHORS
+    assert _fsel(lib, prev=(0, 1, 2, 3, 3)) == ANCHORS
+    assert _fsel(lib, n_cur=5000) == UNSUPPORTED
+    assert _fsel(lib, cam=A + 1) == SHAPE              # bf16 needs 2-byte alignment
+    assert _fsel(lib, dtype=0, act=2 * A + 2) == SHAPE  # fp32 needs 4-byte alignment
+    assert _fsel(lib) == WORKSPACE
+    nb = lib.cast_frame_select_workspace_bytes(4, 64, 64)
+    assert nb > 0 and nb % 256 == 0
+    assert lib.cast_frame_select_workspace_bytes(0, 64, 64) == 0
+    assert lib.cast_frame_select_workspace_bytes(10, 3520, 3072) > nb
