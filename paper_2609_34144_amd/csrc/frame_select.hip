@@ -3,8 +3,9 @@
 //
 // frame_sq      HBM scan: every (control branch, frame) is cut into spans of
 //               kSpan elements; a 256-thread block sums the squares of one span
-//               in fp32 (16-byte loads when the frames allow them) and writes one
-//               partial, so the sums are bit-identical across runs.
+//               in fp32 (four 16-byte loads in flight per thread when the frames
+//               allow them) and writes one partial, so the sums are bit-identical
+//               across runs.
 // frame_select  one block: per present branch r_i = sqrt(sum / (S D)) (partials
 //               added in fp64, fixed order), min / max over the chunk, the
 //               normalised responses and their mean d_i; ages after the block's
@@ -21,7 +22,8 @@ namespace cast {
 namespace {
 
 constexpr int kSqThreads = 256;
-constexpr int kSpan = 16384;          // elements per partial (64 per thread)
+constexpr int kSpan = 32768;          // elements per partial (128 per thread)
+constexpr int kUnroll = 4;            // independent 16-byte loads in flight per thread
 constexpr int kSelThreads = 1024;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -42,13 +44,24 @@ __global__ __launch_bounds__(kSqThreads) void frame_sq_kernel(SqArgs a, float* _
     const float* x = static_cast<const float*>(a.src[z]) + (long long)f * a.frame_elems;
     if constexpr (VEC) {
       const f32x4* x4 = reinterpret_cast<const f32x4*>(x);
-      for (long long e = e0 / 4 + threadIdx.x; e < e1 / 4; e += kSqThreads) {
-        const f32x4 v = __builtin_nontemporal_load(x4 + e);
-        acc = fmaf(v.x, v.x, acc);
-        acc = fmaf(v.y, v.y, acc);
-        acc = fmaf(v.z, v.z, acc);
-        acc = fmaf(v.w, v.w, acc);
+      const long long q1 = e1 / 4;
+      float pa[kUnroll] = {};
+      for (long long e = e0 / 4 + threadIdx.x; e < q1; e += kUnroll * kSqThreads) {
+        f32x4 v[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          const long long eu = e + u * kSqThreads;
+          v[u] = eu < q1 ? __builtin_nontemporal_load(x4 + eu) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          pa[u] = fmaf(v[u].x, v[u].x, pa[u]);
+          pa[u] = fmaf(v[u].y, v[u].y, pa[u]);
+          pa[u] = fmaf(v[u].z, v[u].z, pa[u]);
+          pa[u] = fmaf(v[u].w, v[u].w, pa[u]);
+        }
       }
+      acc = (pa[0] + pa[1]) + (pa[2] + pa[3]);
     } else {
       for (long long e = e0 + threadIdx.x; e < e1; e += kSqThreads) acc = fmaf(x[e], x[e], acc);
     }
@@ -56,16 +69,27 @@ __global__ __launch_bounds__(kSqThreads) void frame_sq_kernel(SqArgs a, float* _
     const uint16_t* x = static_cast<const uint16_t*>(a.src[z]) + (long long)f * a.frame_elems;
     if constexpr (VEC) {
       const u32x4* x8 = reinterpret_cast<const u32x4*>(x);
-      for (long long e = e0 / 8 + threadIdx.x; e < e1 / 8; e += kSqThreads) {
-        const u32x4 v = __builtin_nontemporal_load(x8 + e);
-        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+      const long long q1 = e1 / 8;
+      float pa[kUnroll] = {};
+      for (long long e = e0 / 8 + threadIdx.x; e < q1; e += kUnroll * kSqThreads) {
+        u32x4 v[kUnroll];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const float lo = bf16lo(w[k]), hi = bf16hi(w[k]);
-          acc = fmaf(lo, lo, acc);
-          acc = fmaf(hi, hi, acc);
+        for (int u = 0; u < kUnroll; ++u) {
+          const long long eu = e + u * kSqThreads;
+          v[u] = eu < q1 ? __builtin_nontemporal_load(x8 + eu) : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const float lo = bf16lo(w[k]), hi = bf16hi(w[k]);
+            pa[u] = fmaf(lo, lo, pa[u]);
+            pa[u] = fmaf(hi, hi, pa[u]);
+          }
         }
       }
+      acc = (pa[0] + pa[1]) + (pa[2] + pa[3]);
     } else {
       for (long long e = e0 + threadIdx.x; e < e1; e += kSqThreads) {
         const float v = __uint_as_float((uint32_t)x[e] << 16);
