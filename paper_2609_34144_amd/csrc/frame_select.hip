@@ -7,12 +7,12 @@
 //               allow them) and writes one partial, so the sums are bit-identical
 //               across runs.
 // frame_select  one block: per present branch r_i = sqrt(sum / (S D)) (partials
-//               added in fp64, fixed order), min / max over the chunk, the
-//               normalised responses and their mean d_i; ages after the block's
-//               anchors, coverage debt h_i / ceil(N / K_f), score d_i + lambda D_i
-//               (lambda D_i without a fresh response); the K_f best frames by
-//               rank counting under (score descending, frame ascending), written
-//               in ascending frame order.  Every float operation after r is one
+//               added in fp64 by one wave per frame, fixed order), min / max over
+//               the chunk, the normalised responses and their mean d_i; ages after
+//               the block's anchors, coverage debt h_i / ceil(N / K_f), score
+//               d_i + lambda D_i (lambda D_i without a fresh response); the K_f
+//               best frames by rank counting under (score descending, frame
+//               ascending), written in ascending frame order.  Every float operation after r is one
 //               correctly rounded fp32 operation (no contraction), so the
 //               decision is reproducible on the host in fp32.
 #include "cast_common.h"
@@ -127,16 +127,21 @@ __global__ __launch_bounds__(kSelThreads) void frame_select_kernel(SelArgs a) {
   __shared__ float lohi[2][2];
   const int tid = threadIdx.x, n = a.n_cur;
 
-  // r per present branch (fp64 sum of the partials, in split order)
-  for (int z = 0; z < a.n_present; ++z)
-    for (int i = tid; i < n; i += kSelThreads) {
-      const float* p = a.partial + ((long long)z * n + i) * a.n_split;
-      double s = 0.0;
-      for (int k = 0; k < a.n_split; ++k) s += (double)p[k];
-      const float ri = (float)sqrt(s * a.inv_elems);
+  // r per present branch: one wave per (branch, frame) adds its partials in fp64,
+  // lane l taking partials l, l + 64, ..., then a fixed butterfly
+  const int wave = tid >> 6, lane = tid & 63;
+  for (int item = wave; item < a.n_present * n; item += kSelThreads / 64) {
+    const int z = item / n, i = item - z * n;
+    const float* p = a.partial + (long long)item * a.n_split;
+    double sum = 0.0;
+    for (int k = lane; k < a.n_split; k += 64) sum += (double)p[k];
+    for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+    if (lane == 0) {
+      const float ri = (float)sqrt(sum * a.inv_elems);
       r[z][i] = ri;
       if (a.r_out) a.r_out[(long long)a.row_of[z] * n + i] = ri;
     }
+  }
   __syncthreads();
   // min and max over the chunk, per branch (exact in any order)
   for (int z = 0; z < a.n_present; ++z) {
