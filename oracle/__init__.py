@@ -16,9 +16,10 @@ coupled  reconstruction-coupled historical routing    (Sec. 4.4 eq:omission .. e
                                                        App. B, Algorithm 1)
 frame_select  control-aware frame selection         (Sec. 3.1 eq:sensitivity, Sec. 4.2
                                                        eq:debt, eq:score, App. A.1)
+diagnostics   spectral diagnostics of reconstructions (App. C eq:oracles .. eq:phaseerror)
 
 Every function computes in float64 on the values it is given (bf16-rounded or
 fp32 inputs are widened first), written as the definition in the paper, with
 no blocking or fusion beyond what the definition states.
 """
-from . import route, attn, par, coupled, frame_select  # noqa: F401
+from . import route, attn, par, coupled, frame_select, diagnostics  # noqa: F401

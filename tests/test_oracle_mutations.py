@@ -15,6 +15,8 @@ import oracle.coupled as OC
 import test_oracle_coupled as TC
 import oracle.frame_select as FS
 import test_oracle_frame_select as TFS
+import oracle.diagnostics as DG
+import test_oracle_diagnostics as TDG
 import test_oracle_par as TP
 import test_oracle_route_attn as TR
 
@@ -340,3 +342,63 @@ FS_MUTANTS = {
 def test_frame_select_mutation_caught(name):
     mod = clone(FS, **FS_MUTANTS[name])
     assert _any_pin_fails(mod, TFS.PINS), f"no frame-selection pin catches mutation {name}"
+
+
+# ---- spectral diagnostics
+def _dg_band_no_kappa(ref_t, approx_t, tile_h, tile_w, edges, eps=1e-8):
+    ref = np.asarray(ref_t, dtype=np.float64)
+    err = ref - np.asarray(approx_t, dtype=np.float64)
+    num = np.zeros(len(edges) - 1)
+    for (y0, hp, x0, wp) in P.tiles(ref.shape[0], ref.shape[1], tile_h, tile_w):
+        F = P.rfft2_ortho(err[y0:y0 + hp, x0:x0 + wp])
+        _, _, _, nu = P.bin_tables(hp, wp)
+        e = (np.abs(F) ** 2).sum(axis=2)
+        for k, v in zip(DG.band_index(nu, edges).ravel(), e.ravel()):
+            num[k] += v
+    return num / (num.sum() + eps)
+
+
+def _dg_nrmse_squared(ref_t, approx_t, eps=1e-8):
+    ref = np.asarray(ref_t, dtype=np.float64)
+    d = ref - np.asarray(approx_t, dtype=np.float64)
+    return float((d * d).sum() / ((ref * ref).sum() + eps))
+
+
+def _dg_unwrap_none(phases):
+    return np.asarray(phases, dtype=np.float64).copy()
+
+
+def _dg_corrections_swapped(ref_t, anchor_a, anchor_b, alpha, tile_h, tile_w):
+    rp, rm = DG.oracle_corrections(ref_t, anchor_a, anchor_b, alpha, tile_h, tile_w)
+    return rm, rp
+
+
+def _dg_phase_error_amplitude_weight(ref_t, anchor_a, theta_tiles, alpha, tile_h, tile_w, eps=1e-8):
+    ref = np.asarray(ref_t, dtype=np.float64)
+    anc = np.asarray(anchor_a, dtype=np.float64)
+    num = den = 0.0
+    for p, (y0, hp, x0, wp) in enumerate(P.tiles(ref.shape[0], ref.shape[1], tile_h, tile_w)):
+        Ft = P.rfft2_ortho(ref[y0:y0 + hp, x0:x0 + wp])
+        Fa = P.rfft2_ortho(anc[y0:y0 + hp, x0:x0 + wp])
+        _, _, kappa, _ = P.bin_tables(hp, wp)
+        w = kappa[:, :, None] * np.abs(Ft)
+        w = np.where((np.abs(Ft) > 0) & (np.abs(Fa) > 0), w, 0.0)
+        x = np.angle(Ft) - np.angle(Fa) - alpha * np.asarray(theta_tiles[p])[:, :, None]
+        num += float((w * np.abs(DG.wrap_pm_pi(x))).sum())
+        den += float(w.sum())
+    return num / (den + eps)
+
+
+DG_MUTANTS = {
+    "band_no_kappa": dict(band_energy=_dg_band_no_kappa),
+    "nrmse_squared": dict(nrmse=_dg_nrmse_squared),
+    "no_unwrap": dict(unwrap_track=_dg_unwrap_none),
+    "corrections_swapped": dict(oracle_corrections=_dg_corrections_swapped),
+    "phase_error_amplitude_weight": dict(phase_error=_dg_phase_error_amplitude_weight),
+}
+
+
+@pytest.mark.parametrize("name", sorted(DG_MUTANTS))
+def test_diagnostics_mutation_caught(name):
+    mod = clone(DG, **DG_MUTANTS[name])
+    assert _any_pin_fails(mod, TDG.PINS), f"no diagnostics pin catches mutation {name}"
