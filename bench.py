@@ -323,6 +323,30 @@ def main():
         sel_ms = float(np.mean([a.elapsed_time(b) for a, b in sm]))
         del ctl
 
+    # spectral diagnostics of the skipped frames (validation, not inference): error
+    # ratio, band energies, transport phase error and both oracle corrections
+    diag_ms = None
+    if w.has_par:
+        s1, _ = cast.par_debug_shapes(w.n_a, w.Hg, w.Wg, prm)
+        theta = torch.zeros(s1, device=dev)
+        s0 = sets[0]
+        cast.cast_par_reconstruct(s0["resid"], w.anchors, cast.cast_par_params_default(),
+                                  out=s0["x"], theta_out=theta, workspace=par_ws, stream=stream)
+        dws = torch.empty(cast.cast_spectral_diagnostics_workspace_bytes(
+            w.n_frames, w.Hg, w.Wg, w.D, cast.cast_diag_params_default()), dtype=torch.uint8, device=dev)
+        dm = [ev(), ev()]
+        n_diag = 3
+        cast.cast_spectral_diagnostics(s0["resid"], s0["x"], w.anchors, theta=theta,
+                                       want_corrections=True, workspace=dws, stream=stream)
+        torch.cuda.synchronize()
+        dm[0].record(stream)
+        for _ in range(n_diag):
+            cast.cast_spectral_diagnostics(s0["resid"], s0["x"], w.anchors, theta=theta,
+                                           want_corrections=True, workspace=dws, stream=stream)
+        dm[1].record(stream)
+        torch.cuda.synchronize()
+        diag_ms = dm[0].elapsed_time(dm[1]) / n_diag
+
     value = w.frame_tokens / (ms_step / 1e3)
     res = {
         "metric": "CAST block-step frame-tokens/s (routing + routed anchor attention + PAR)",
@@ -336,7 +360,7 @@ def main():
                    "par_mode": "accumulate", "input_copies": N_COPIES},
         "per_call_ms": {"route": route_ms, "attn": attn_ms, "par": par_ms,
                         "route_coupled": coupled_ms, "par_block_update": block_ms,
-                        "frame_select": sel_ms},
+                        "frame_select": sel_ms, "spectral_diagnostics": diag_ms},
     }
     extra = {}
     traffic = load_traffic(w.name)

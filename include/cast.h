@@ -334,6 +334,62 @@ cast_status_t cast_frame_select(const void* delta_cam, const void* delta_act, in
                                 float* r_out, float* score_out, int32_t* anchors_out,
                                 void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Spectral diagnostics of reconstructed residuals (App. C eq:oracles,
+ * eq:bandenergy, eq:phaseerror; the relative error e_t of Sec. 3.1
+ * eq:sensitivity).  Reference-based: for validation, not for inference.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int tile_h, tile_w;       /* the PAR tiling (disjoint tiles, edge tiles at their own size): 8, 8 */
+  int n_bands;              /* radial bands, 1 .. 8 */
+  float band_edges[9];      /* ascending, band_edges[0] = 0, band_edges[n_bands] = 1: band k holds
+                               the bins with band_edges[k] <= nu < band_edges[k+1] (nu = PAR's
+                               normalised radius; nu = 1 falls in the last band) */
+  float eps;                /* 1e-8 */
+} cast_diag_params_t;
+
+/* 8x8 tiles, three bands with edges (0, 1/3, 2/3, 1), eps = 1e-8. */
+void cast_diag_params_default(cast_diag_params_t* p);
+
+/* Device scratch (bytes) needed by cast_spectral_diagnostics. */
+size_t cast_spectral_diagnostics_workspace_bytes(int n_frames, int Hg, int Wg, int D,
+                                                 const cast_diag_params_t* params);
+
+/*
+ * For every skipped frame t of eq:block (pair (a, b), alpha = (t - a)/(b - a)):
+ *   nrmse_out[t]  = ||R_t - R_hat_t|| / (||R_t|| + eps) over the frame;
+ *   band_out[t,k] = sum_{tiles, channels, bins in band k} kappa |F_t - F_hat_t|^2
+ *                   / (sum over all bins + eps)                        (eq:bandenergy);
+ *   phase_err_out[t] = sum w |wrap_[-pi,pi)(Arg F_t - Arg F_a - alpha theta_p)| / (sum w + eps),
+ *                   w = kappa |F_t|^2 on bins where F_t and F_a are nonzero    (eq:phaseerror);
+ *   r_phase_out[t], r_mag_out[t] = inverse transforms of |F_lin| e^{i Arg F_t} and
+ *                   |F_t| e^{i Arg F_lin}, F_lin = (1 - alpha) F_a + alpha F_b  (eq:oracles).
+ * F is the orthonormal real 2-D DFT per tile and channel, kappa the real-FFT
+ * multiplicity (1 on the columns that hold their own conjugates, 2 elsewhere).
+ * Entries of anchor frames are 0; r_phase_out / r_mag_out slots of anchors are not
+ * written.
+ *
+ * ref      fp32 [n_frames, Hg, Wg, D] device: reference residuals of every frame
+ *          (anchors included).
+ * approx   fp32 [n_frames, Hg, Wg, D] device: the reconstructions R_hat_t (skipped
+ *          slots read; e.g. the output of cast_par_reconstruct in write mode).
+ * theta    fp32 [n_anchor - 1, tiles, tile_h * (tile_w/2 + 1)] device: the transport
+ *          phases of the pairs (theta_out of cast_par_reconstruct with the same
+ *          tiling), or NULL: then phase_err_out is not written.
+ * anchors  HOST int[n_anchor], strictly increasing in [0, n_frames), n_anchor >= 2.
+ * nrmse_out [n_frames], band_out [n_frames, n_bands], phase_err_out [n_frames],
+ *          r_phase_out, r_mag_out [n_frames, Hg, Wg, D]: device, each may be NULL.
+ * Errors: CAST_ERR_NULL (ref, approx, anchors, params), CAST_ERR_SHAPE (sizes,
+ * bands, misaligned buffers), CAST_ERR_ANCHORS, CAST_ERR_UNSUPPORTED (tile edges
+ * above 8, n_frames > 4096, n_anchor > 512), CAST_ERR_WORKSPACE.
+ */
+cast_status_t cast_spectral_diagnostics(const float* ref, const float* approx, const float* theta,
+                                        const int* anchors, int n_anchor, int n_frames, int Hg,
+                                        int Wg, int D, const cast_diag_params_t* params,
+                                        float* nrmse_out, float* band_out, float* phase_err_out,
+                                        float* r_phase_out, float* r_mag_out, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -26,7 +26,8 @@ EXPORTED = ["cast_status_string", "cast_last_error_detail", "cast_abi_version",
             "cast_par_params_default", "cast_par_workspace_bytes", "cast_par_reconstruct",
             "cast_coupled_params_default", "cast_wo_gram", "cast_route_coupled_workspace_bytes",
             "cast_route_coupled", "cast_select_params_default",
-            "cast_frame_select_workspace_bytes", "cast_frame_select"]
+            "cast_frame_select_workspace_bytes", "cast_frame_select", "cast_diag_params_default",
+            "cast_spectral_diagnostics_workspace_bytes", "cast_spectral_diagnostics"]
 
 
 class CastError(RuntimeError):
@@ -55,6 +56,12 @@ class CoupledParams(ctypes.Structure):
 class SelectParams(ctypes.Structure):
     """cast_select_params_t (include/cast.h)."""
     _fields_ = [("lambda_cov", ctypes.c_float), ("eps", ctypes.c_float)]
+
+
+class DiagParams(ctypes.Structure):
+    """cast_diag_params_t (include/cast.h)."""
+    _fields_ = [("tile_h", ctypes.c_int), ("tile_w", ctypes.c_int), ("n_bands", ctypes.c_int),
+                ("band_edges", ctypes.c_float * 9), ("eps", ctypes.c_float)]
 
 
 _lib = None
@@ -108,6 +115,14 @@ def load(path: str = LIB_PATH):
     lib.cast_frame_select.restype = _i
     lib.cast_frame_select.argtypes = [_vp, _vp, _i, _i, _i, _i, _c.POINTER(_i), _i, _i,
                                       _c.POINTER(SelectParams), _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.cast_diag_params_default.restype = None
+    lib.cast_diag_params_default.argtypes = [_c.POINTER(DiagParams)]
+    lib.cast_spectral_diagnostics_workspace_bytes.restype = _sz
+    lib.cast_spectral_diagnostics_workspace_bytes.argtypes = [_i, _i, _i, _i, _c.POINTER(DiagParams)]
+    lib.cast_spectral_diagnostics.restype = _i
+    lib.cast_spectral_diagnostics.argtypes = [_vp, _vp, _vp, _c.POINTER(_i), _i, _i, _i, _i, _i,
+                                              _c.POINTER(DiagParams), _vp, _vp, _vp, _vp, _vp,
+                                              _vp, _sz, _vp]
     _lib = lib
     return lib
 
@@ -275,6 +290,46 @@ def cast_frame_select(delta_cam, delta_act, anchors_prev, k_f: int, ages,
                                  _ptr(score_out), _ptr(anchors_out), _ptr(ws), wsb,
                                  _stream(stream)))
     return anchors_out
+
+
+def cast_diag_params_default(band_edges=None, **overrides) -> DiagParams:
+    p = DiagParams()
+    load().cast_diag_params_default(ctypes.byref(p))
+    for k, v in overrides.items():
+        setattr(p, k, v)
+    if band_edges is not None:
+        p.n_bands = len(band_edges) - 1
+        for k, e in enumerate(band_edges):
+            p.band_edges[k] = float(e)
+    return p
+
+
+def cast_spectral_diagnostics(ref, approx, anchors, params: DiagParams | None = None, theta=None,
+                              want_corrections: bool = False, workspace=None, stream=None):
+    """Spectral diagnostics of the skipped frames.  ref, approx fp32 [n_frames, Hg,
+    Wg, D] (device); theta: PAR's theta_out for the same anchors and tiling, or None.
+    Returns dict(nrmse [n_frames], bands [n_frames, n_bands], phase_err [n_frames]
+    or None, r_phase, r_mag [n_frames, Hg, Wg, D] or None)."""
+    import torch
+    lib = load()
+    if params is None:
+        params = cast_diag_params_default()
+    n_frames, Hg, Wg, D = ref.shape
+    dev = ref.device
+    nrmse = torch.zeros(n_frames, dtype=torch.float32, device=dev)
+    bands = torch.zeros((n_frames, params.n_bands), dtype=torch.float32, device=dev)
+    perr = torch.zeros(n_frames, dtype=torch.float32, device=dev) if theta is not None else None
+    rp = torch.zeros_like(ref) if want_corrections else None
+    rm = torch.zeros_like(ref) if want_corrections else None
+    anc = [int(a) for a in anchors]
+    arr = (ctypes.c_int * max(len(anc), 1))(*anc)
+    nb = lib.cast_spectral_diagnostics_workspace_bytes(n_frames, Hg, Wg, D, ctypes.byref(params))
+    ws, wsb = _ws(nb, dev, workspace)
+    _check(lib.cast_spectral_diagnostics(_ptr(ref), _ptr(approx), _ptr(theta), arr, len(anc),
+                                         n_frames, Hg, Wg, D, ctypes.byref(params), _ptr(nrmse),
+                                         _ptr(bands), _ptr(perr), _ptr(rp), _ptr(rm), _ptr(ws), wsb,
+                                         _stream(stream)))
+    return {"nrmse": nrmse, "bands": bands, "phase_err": perr, "r_phase": rp, "r_mag": rm}
 
 
 def cast_anchor_attn(q, k_hist, v_hist, idx, k_eff: int, scale: float, k_cur=None, v_cur=None,

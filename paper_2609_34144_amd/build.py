@@ -38,6 +38,7 @@ UNITS = [("par.hip", "par", ["-fno-signed-zeros"])] + [
     ("route_kv.hip", "route_kv", []),
     ("route_coupled.hip", "route_coupled", []),
     ("frame_select.hip", "frame_select", []),
+    ("diag.hip", "diag", []),
     ("capi.hip", "capi", []),
 ]
 

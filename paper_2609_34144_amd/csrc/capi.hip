@@ -348,4 +348,69 @@ cast_status_t cast_frame_select(const void* delta_cam, const void* delta_act, in
                              static_cast<float*>(workspace), stream);
 }
 
+// ---------------------------------------------------------------------------
+// Spectral diagnostics
+// ---------------------------------------------------------------------------
+void cast_diag_params_default(cast_diag_params_t* p) {
+  if (p == nullptr) return;
+  p->tile_h = 8;
+  p->tile_w = 8;
+  p->n_bands = 3;
+  for (int k = 0; k < 9; ++k) p->band_edges[k] = 0.0f;
+  p->band_edges[1] = 1.0f / 3.0f;
+  p->band_edges[2] = 2.0f / 3.0f;
+  p->band_edges[3] = 1.0f;
+  p->eps = 1e-8f;
+}
+
+static cast_status_t diag_check(int n_frames, int Hg, int Wg, int D, const cast_diag_params_t* p) {
+  if (p == nullptr) return fail(CAST_ERR_NULL, "diag: params is NULL");
+  if (n_frames < 1 || Hg < 1 || Wg < 1 || D < 1) return fail(CAST_ERR_SHAPE, "diag: sizes must be >= 1");
+  if (n_frames > kParMaxFrames) return fail(CAST_ERR_UNSUPPORTED, "diag: n_frames > %d", kParMaxFrames);
+  if (p->tile_h < 1 || p->tile_h > kParMaxTile || p->tile_w < 1 || p->tile_w > kParMaxTile)
+    return fail(CAST_ERR_UNSUPPORTED, "diag: tile edges must be in [1, %d]", kParMaxTile);
+  if (p->n_bands < 1 || p->n_bands > kDiagMaxBands)
+    return fail(CAST_ERR_SHAPE, "diag: n_bands must be in [1, %d]", kDiagMaxBands);
+  if (p->band_edges[0] != 0.0f || p->band_edges[p->n_bands] != 1.0f)
+    return fail(CAST_ERR_SHAPE, "diag: band edges must start at 0 and end at 1");
+  for (int k = 0; k < p->n_bands; ++k)
+    if (!(p->band_edges[k + 1] > p->band_edges[k])) return fail(CAST_ERR_SHAPE, "diag: band edges must increase");
+  if (!(p->eps >= 0.0f)) return fail(CAST_ERR_SHAPE, "diag: eps must be >= 0");
+  if ((long long)Hg * Wg * D >= (1LL << 30)) return fail(CAST_ERR_UNSUPPORTED, "diag: frame too large");
+  return CAST_OK;
+}
+
+size_t cast_spectral_diagnostics_workspace_bytes(int n_frames, int Hg, int Wg, int D,
+                                                 const cast_diag_params_t* params) {
+  if (diag_check(n_frames, Hg, Wg, D, params) != CAST_OK) return 0;
+  return diag_workspace_bytes(n_frames, Hg, Wg, D, params->tile_h, params->tile_w);
+}
+
+cast_status_t cast_spectral_diagnostics(const float* ref, const float* approx, const float* theta,
+                                        const int* anchors, int n_anchor, int n_frames, int Hg,
+                                        int Wg, int D, const cast_diag_params_t* params,
+                                        float* nrmse_out, float* band_out, float* phase_err_out,
+                                        float* r_phase_out, float* r_mag_out, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream) {
+  if (ref == nullptr || approx == nullptr || anchors == nullptr)
+    return fail(CAST_ERR_NULL, "diag: ref, approx and anchors are required");
+  cast_status_t st = diag_check(n_frames, Hg, Wg, D, params);
+  if (st != CAST_OK) return st;
+  if (n_anchor < 2 || n_anchor > n_frames || n_anchor > kParMaxAnchors)
+    return fail(CAST_ERR_ANCHORS, "diag: need 2 <= n_anchor <= min(n_frames, %d)", kParMaxAnchors);
+  for (int j = 0; j < n_anchor; ++j) {
+    if (anchors[j] < 0 || anchors[j] >= n_frames)
+      return fail(CAST_ERR_ANCHORS, "diag: anchor %d = %d outside [0, %d)", j, anchors[j], n_frames);
+    if (j > 0 && anchors[j] <= anchors[j - 1])
+      return fail(CAST_ERR_ANCHORS, "diag: anchors must be strictly increasing (index %d)", j);
+  }
+  const void* bufs[] = {ref, approx, theta, nrmse_out, band_out, phase_err_out, r_phase_out, r_mag_out};
+  for (const void* b : bufs)
+    if (!aligned(b, 4)) return fail(CAST_ERR_SHAPE, "diag: misaligned buffers");
+  st = check_ws(workspace, workspace_bytes, diag_workspace_bytes(n_frames, Hg, Wg, D, params->tile_h, params->tile_w));
+  if (st != CAST_OK) return st;
+  return launch_diag(ref, approx, theta, anchors, n_anchor, n_frames, Hg, Wg, D, *params,
+                     nrmse_out, band_out, phase_err_out, r_phase_out, r_mag_out, workspace, stream);
+}
+
 }  // extern "C"

@@ -120,4 +120,15 @@ cast_status_t launch_frame_select(const void* cam, const void* act, int dtype, i
                                   float* score_out, int32_t* anchors_out, float* partial,
                                   hipStream_t stream);
 
+// ---------------------------------------------------------------------------
+// Spectral diagnostics
+// ---------------------------------------------------------------------------
+constexpr int kDiagMaxBands = 8;
+size_t diag_workspace_bytes(int n_frames, int Hg, int Wg, int D, int tile_h, int tile_w);
+cast_status_t launch_diag(const float* ref, const float* approx, const float* theta,
+                          const int* anchors, int n_anchor, int n_frames, int Hg, int Wg, int D,
+                          const cast_diag_params_t& p, float* nrmse_out, float* band_out,
+                          float* phase_err_out, float* r_phase_out, float* r_mag_out, void* ws,
+                          hipStream_t stream);
+
 }  // namespace cast

@@ -3,6 +3,8 @@ include/cast.h declares, and each entry point rejects invalid arguments with the
 documented status before enqueueing anything (all checks here return before any
 HIP call).  Bypass rules of App. A.1 / App. B.3 return OK without work."""
 import ctypes
+
+import numpy as np
 import os
 import re
 import subprocess
@@ -271,3 +273,36 @@ def test_frame_select_validation(lib):
     assert nb > 0 and nb % 256 == 0
     assert lib.cast_frame_select_workspace_bytes(0, 64, 64) == 0
     assert lib.cast_frame_select_workspace_bytes(10, 3520, 3072) > nb
+
+
+# ---- spectral diagnostics
+def test_diag_params_default(lib):
+    p = cast.cast_diag_params_default()
+    assert (p.tile_h, p.tile_w, p.n_bands) == (8, 8, 3)
+    assert list(p.band_edges)[:4] == [0.0, np.float32(1 / 3), np.float32(2 / 3), 1.0]
+    assert abs(p.eps - 1e-8) < 1e-14
+
+
+def _diag(lib, *, ref=A, approx=2 * A, theta=None, anchors=(0, 3), n_frames=4, Hg=8, Wg=8, D=64,
+          params=None, ws=None, wsb=0, **pkw):
+    p = params if params is not None else cast.cast_diag_params_default(**pkw)
+    arr = (ctypes.c_int * max(len(anchors), 1))(*anchors)
+    return lib.cast_spectral_diagnostics(ref, approx, theta, arr, len(anchors), n_frames, Hg, Wg, D,
+                                         ctypes.byref(p), None, None, None, None, None, ws, wsb, None)
+
+
+def test_diag_validation(lib):
+    assert _diag(lib, ref=None) == NULL
+    assert _diag(lib, anchors=(1,)) == ANCHORS
+    assert _diag(lib, anchors=(3, 1)) == ANCHORS
+    assert _diag(lib, anchors=(0, 4)) == ANCHORS
+    assert _diag(lib, tile_h=9) == UNSUPPORTED
+    assert _diag(lib, n_bands=0) == SHAPE
+    assert _diag(lib, band_edges=[0.0, 0.6, 0.5, 1.0]) == SHAPE
+    assert _diag(lib, band_edges=[0.1, 1.0]) == SHAPE
+    assert _diag(lib, band_edges=[0.0, 0.9]) == SHAPE
+    assert _diag(lib, approx=2 * A + 2) == SHAPE
+    assert _diag(lib) == WORKSPACE
+    p = cast.cast_diag_params_default()
+    nb = lib.cast_spectral_diagnostics_workspace_bytes(4, 8, 8, 64, ctypes.byref(p))
+    assert nb > 0 and nb % 256 == 0

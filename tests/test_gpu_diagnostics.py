@@ -1,0 +1,112 @@
+"""GPU parity of the spectral diagnostics (cast_spectral_diagnostics) against the
+oracle (oracle/diagnostics.py) on identical inputs: generator ground-truth
+residuals of every frame as the reference, the GPU PAR reconstruction (write mode)
+as the approximation, and each side's own PAR transport phases.
+
+Bars (fp32 tile DFTs of at most 8x8 points and fp32 per-lane sums, against
+float64): e_t relative 1e-4; band fractions 1e-5 absolute; transport phase error
+1e-4 absolute; oracle corrections rel-RMS 1e-5 over each frame."""
+import numpy as np
+import pytest
+import torch
+
+import gen
+from gen import workloads as W
+from oracle import diagnostics as DG
+from oracle import par as OP
+from test_gpu_parity import log, rel_rms
+
+pytestmark = pytest.mark.gpu
+
+NRMSE_REL, BAND_ABS, PHASE_ABS, CORR_RMS = 1e-4, 1e-5, 1e-4, 1e-5
+
+
+def run_case(cast_lib, ref_np, anchors, label, tile=8, edges=(0.0, 1 / 3, 2 / 3, 1.0), corr=True):
+    dev = "cuda"
+    edges = [float(np.float32(e)) for e in edges]      # the values the kernel sees
+    ref = torch.from_numpy(ref_np.astype(np.float32)).to(dev)
+    prm = cast_lib.cast_par_params_default(tile_h=tile, tile_w=tile)
+    s1, _ = cast_lib.par_debug_shapes(len(anchors), ref.shape[1], ref.shape[2], prm)
+    theta = torch.zeros(s1, device=dev)
+    approx = torch.zeros_like(ref)
+    cast_lib.cast_par_reconstruct(ref, anchors, prm, out=approx, theta_out=theta)
+    dprm = cast_lib.cast_diag_params_default(band_edges=edges, tile_h=tile, tile_w=tile)
+    got = cast_lib.cast_spectral_diagnostics(ref, approx, anchors, dprm, theta=theta,
+                                             want_corrections=corr)
+    torch.cuda.synchronize()
+    ref64 = ref.cpu().numpy().astype(np.float64)
+    app64 = approx.cpu().numpy().astype(np.float64)
+    want = DG.frame_diagnostics(ref64, app64, anchors, OP.ParParams(tile_h=tile, tile_w=tile), edges)
+    nr = got["nrmse"].cpu().numpy()
+    bd = got["bands"].cpu().numpy()
+    pe = got["phase_err"].cpu().numpy()
+    worst = dict(nrmse=0.0, bands=0.0, phase=0.0, corr=0.0)
+    for t in range(ref.shape[0]):
+        if t in anchors:
+            assert nr[t] == 0.0 and not bd[t].any() and pe[t] == 0.0
+            continue
+        w = want[t]
+        worst["nrmse"] = max(worst["nrmse"], abs(nr[t] - w["nrmse"]) / max(w["nrmse"], 1e-30))
+        worst["bands"] = max(worst["bands"], float(np.abs(bd[t] - w["bands"]).max()))
+        worst["phase"] = max(worst["phase"], abs(pe[t] - w["phase_err"]))
+        if corr:
+            worst["corr"] = max(worst["corr"], rel_rms(got["r_phase"][t].cpu().numpy(), w["r_phase"]),
+                                rel_rms(got["r_mag"][t].cpu().numpy(), w["r_mag"]))
+    log(f"[diag {label}] worst: e_t rel {worst['nrmse']:.2e}, bands {worst['bands']:.2e}, "
+        f"phase {worst['phase']:.2e}, corrections rel-RMS {worst['corr']:.2e}; "
+        f"e_t {[round(float(nr[t]), 4) for t in range(len(nr)) if t not in anchors]}, "
+        f"phase error {[round(float(pe[t]), 4) for t in range(len(pe)) if t not in anchors]}")
+    assert worst["nrmse"] <= NRMSE_REL and worst["bands"] <= BAND_ABS
+    assert worst["phase"] <= PHASE_ABS and worst["corr"] <= CORR_RMS, worst
+    if corr:   # anchor slots of the corrections are not written
+        for a in anchors:
+            assert not got["r_phase"][a].any() and not got["r_mag"][a].any()
+    return got
+
+
+def test_diag_translation(cast_lib):
+    """A coherent constant-velocity translation (eq:shift) over a 32x32 frame with
+    8x8 tiles: every frame is R_0 shifted by t d, so PAR's reconstruction is close
+    and the transport phase error small; the linear interpolation is the baseline."""
+    rng = np.random.default_rng(4)
+    from gen.workloads import fourier_shift, power_law_field
+    base = power_law_field(32, 32, 48, 2.0, rng)
+    d = np.array([0.3, -0.2])
+    ref = np.stack([fourier_shift(base, d * t) for t in range(6)])
+    got = run_case(cast_lib, ref, (0, 3, 5), "translation")
+    assert float(got["nrmse"][1]) < 0.5
+
+
+def test_diag_edges_and_bands(cast_lib):
+    """Edge tiles of every kind, boundary extrapolation on both sides, four bands,
+    channels not a multiple of the 64-lane block, a 4x4 tiling."""
+    rng = np.random.default_rng(11)
+    for (n, Hg, Wg, D, anchors, tile) in [(7, 14, 13, 80, (2, 5), 8), (5, 11, 11, 16, (0, 1, 3), 4)]:
+        base = rng.standard_normal((Hg, Wg, D))
+        ref = np.stack([np.roll(base, (t, 2 * t), axis=(0, 1)) + 0.3 * rng.standard_normal((Hg, Wg, D))
+                        for t in range(n)])
+        run_case(cast_lib, ref, anchors, f"{Hg}x{Wg}x{D} tile{tile}", tile=tile,
+                 edges=(0.0, 0.25, 0.5, 0.75, 1.0))
+
+
+def test_diag_matrix_like(cast_lib):
+    """The Matrix-Game-like block with the generator's ground-truth skipped frames."""
+    w = gen.get(W.MATRIX)
+    ref, _, _ = gen.par_inputs(w, seed=42, frames="all")
+    run_case(cast_lib, ref, w.anchors, "matrix")
+
+
+def test_diag_without_theta(cast_lib):
+    w = gen.get(W.TINY)
+    ref_np, _, _ = gen.par_inputs(w, seed=3, frames="all")
+    ref = torch.from_numpy(ref_np.astype(np.float32)).to("cuda")
+    approx = torch.zeros_like(ref)
+    cast_lib.cast_par_reconstruct(ref, w.anchors, cast_lib.cast_par_params_default(), out=approx)
+    got = cast_lib.cast_spectral_diagnostics(ref, approx, w.anchors)
+    torch.cuda.synchronize()
+    assert got["phase_err"] is None and got["r_phase"] is None
+    want = DG.frame_diagnostics(ref.cpu().numpy().astype(np.float64), approx.cpu().numpy().astype(np.float64),
+                                w.anchors, OP.ParParams(), [0.0, float(np.float32(1 / 3)),
+                                                            float(np.float32(2 / 3)), 1.0])
+    for t, v in want.items():
+        assert abs(got["nrmse"][t].item() - v["nrmse"]) <= NRMSE_REL * v["nrmse"]
