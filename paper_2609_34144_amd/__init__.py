@@ -304,6 +304,10 @@ def cast_diag_params_default(band_edges=None, **overrides) -> DiagParams:
     return p
 
 
+def cast_spectral_diagnostics_workspace_bytes(n_frames, Hg, Wg, D, params: DiagParams) -> int:
+    return load().cast_spectral_diagnostics_workspace_bytes(n_frames, Hg, Wg, D, ctypes.byref(params))
+
+
 def cast_spectral_diagnostics(ref, approx, anchors, params: DiagParams | None = None, theta=None,
                               want_corrections: bool = False, workspace=None, stream=None):
     """Spectral diagnostics of the skipped frames.  ref, approx fp32 [n_frames, Hg,

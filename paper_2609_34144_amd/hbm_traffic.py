@@ -36,8 +36,10 @@ KERNEL_SOURCES = {
 
 
 def sources_hash(part: str) -> str:
+    """Hash of the sources that define the part's kernels (the shared header holds
+    only declarations and constants and is left out)."""
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES[part] + ["cast_common.h"]:
+    for f in KERNEL_SOURCES[part]:
         with open(os.path.join(HERE, "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

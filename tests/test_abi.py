@@ -306,3 +306,10 @@ def test_diag_validation(lib):
     p = cast.cast_diag_params_default()
     nb = lib.cast_spectral_diagnostics_workspace_bytes(4, 8, 8, 64, ctypes.byref(p))
     assert nb > 0 and nb % 256 == 0
+
+
+def test_binding_wraps_every_entry_point():
+    """The Python binding carries every C entry point under its own name."""
+    missing = [n for n in cast.EXPORTED
+               if n not in ("cast_status_string", "cast_last_error_detail") and not hasattr(cast, n)]
+    assert not missing, missing
