@@ -184,6 +184,26 @@ def test_attn_shapes_and_ragged_tails(cast_lib, dh):
     check_attn(cast_lib, q, k, v, idx, 3, 1 / math.sqrt(dh), label=f"hist-only dh{dh}")
 
 
+@pytest.mark.parametrize("dh", [32, 64, 128])
+def test_attn_fast_and_aligned_modes(cast_lib, dh):
+    """History-only sequences whose chunks have >= 64 rows: chunks that are not a
+    multiple of the 64-key tile (tiles straddle two chunks), chunks that are (no
+    tile straddles), and a single routed chunk; ragged query tails; routed
+    indices in arbitrary order with a repeated chunk."""
+    torch.manual_seed(100 + dh)
+    dev = "cuda"
+    for (S, M, Bv, idx_rows) in [(300, 5, 100, [[4, 0, 2], [1, 1, 3]]),
+                                 (270, 6, 128, [[5, 2, 0], [3, 4, 1]]),
+                                 (70, 3, 64, [[2], [0]])]:
+        n_a, H = 1, 2
+        q = torch.randn(n_a, S, H, dh, device=dev).to(torch.bfloat16)
+        k = torch.randn(M, Bv, H, dh, device=dev).to(torch.bfloat16)
+        v = torch.randn(M, Bv, H, dh, device=dev).to(torch.bfloat16)
+        idx = torch.tensor([idx_rows], dtype=torch.int32, device=dev)
+        check_attn(cast_lib, q, k, v, idx, idx.shape[2], 1 / math.sqrt(dh),
+                   label=f"modes dh{dh} Bv{Bv}")
+
+
 def test_attn_topk_all_equals_dense(cast_lib):
     """topk = M routes every chunk: the result is dense attention over the whole history."""
     w = gen.get(W.TINY)
