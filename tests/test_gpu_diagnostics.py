@@ -110,3 +110,14 @@ def test_diag_without_theta(cast_lib):
                                                             float(np.float32(2 / 3)), 1.0])
     for t, v in want.items():
         assert abs(got["nrmse"][t].item() - v["nrmse"]) <= NRMSE_REL * v["nrmse"]
+
+
+def test_diag_one_and_eight_bands(cast_lib):
+    """The band bookkeeping at its limits: one band (all the error) and eight."""
+    rng = np.random.default_rng(12)
+    base = rng.standard_normal((16, 16, 8))
+    ref = np.stack([np.roll(base, (t, -t), axis=(0, 1)) + 0.2 * rng.standard_normal((16, 16, 8))
+                    for t in range(4)])
+    got = run_case(cast_lib, ref, (0, 3), "one band", edges=(0.0, 1.0), corr=False)
+    assert np.allclose(got["bands"][1:3].cpu().numpy(), 1.0, atol=1e-6)
+    run_case(cast_lib, ref, (0, 3), "eight bands", edges=tuple(np.linspace(0.0, 1.0, 9)), corr=False)

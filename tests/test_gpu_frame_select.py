@@ -140,3 +140,15 @@ def test_select_deterministic(cast_lib):
         torch.cuda.synchronize()
         outs.append((a.clone(), s.clone(), ages.clone()))
     assert all(torch.equal(x, y) for x, y in zip(outs[0], outs[1]))
+
+
+def test_select_single_frame_and_single_anchor(cast_lib):
+    """N_cur = 1 (the one frame is always the anchor; its normalised response is 0)
+    and K_f = 1 of several frames (the strongest response wins)."""
+    w = W.Workload(**{**gen.get(W.TINY).__dict__, "Hg": 4, "Wg": 4, "D_par": 8})
+    for n, k in ((1, 1), (6, 1)):
+        cam, act = gen.control_inputs(w, seed=21 + n, device="cuda", n_cur=n)
+        ages = torch.zeros(n, dtype=torch.int32, device="cuda")
+        got, _, _ = one_step(cast_lib, cam, act, [0], k, ages, np.zeros(n, dtype=np.int64), f"n{n} k{k}")
+        if n == 1:
+            assert got == [0]
