@@ -187,9 +187,11 @@ def main():
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
 
-    # ---- inputs (resident in HBM), N_COPIES copies at distinct addresses
-    q, k, v, kc, vc = gen.attn_inputs(w, seed=args.seed, device=dev) if w.has_attention else \
-        (None,) * 5
+    # ---- inputs (resident in HBM), N_COPIES copies at distinct addresses.  The
+    # attention inputs of copy c come from seed SEEDS[c] (the base seed, then the
+    # timing repeats 0, 1, 2), so the steps cycle over different routings; PAR's
+    # work does not depend on the values, and its copies are clones of one draw.
+    seeds = [args.seed] + [s for s in (0, 1, 2) if s != args.seed][:N_COPIES - 1]
     resid_np, _, _ = gen.par_inputs(w, seed=args.seed)
     resid = torch.from_numpy(resid_np).to(dev)
     del resid_np
@@ -197,9 +199,11 @@ def main():
     for c in range(N_COPIES):
         s = {"resid": resid.clone(), "x": torch.randn(resid.shape, device=dev, dtype=torch.float32)}
         if w.has_attention:
-            s.update(q=q.clone(), k=k.clone(), v=v.clone())
+            q, k, v, _, _ = gen.attn_inputs(w, seed=seeds[c % len(seeds)], device=dev)
+            s.update(q=q, k=k, v=v)
+            del q, k, v
         sets.append(s)
-    del q, k, v, resid
+    del resid
     prm = cast.cast_par_params_default(accumulate=1)
     k_eff = min(w.topk, w.M) if w.has_attention else 0
     route_ws = par_ws = None
@@ -256,9 +260,10 @@ def main():
     for i in range(args.steps):
         step(sets[i % N_COPIES], marks[i])
     torch.cuda.synchronize()
-    route_ms = float(np.mean([m[0].elapsed_time(m[1]) for m in marks]))
-    attn_ms = float(np.mean([m[1].elapsed_time(m[2]) for m in marks]))
-    par_ms = float(np.mean([m[2].elapsed_time(m[3]) for m in marks]))
+    per_call = {"route": [m[0].elapsed_time(m[1]) for m in marks],
+                "attn": [m[1].elapsed_time(m[2]) for m in marks],
+                "par": [m[2].elapsed_time(m[3]) for m in marks]}
+    route_ms, attn_ms, par_ms = (float(np.mean(per_call[c])) for c in ("route", "attn", "par"))
 
     # reconstruction-coupled routing (NEXT-1), timed on its own after the step;
     # the W_O Gram matrices depend on weights only and are prepared once, untimed
@@ -283,7 +288,8 @@ def main():
                                     w.scale, params=cprm, idx_out=cidx, workspace=cws, stream=stream)
             cm[i][1].record(stream)
         torch.cuda.synchronize()
-        coupled_ms = float(np.mean([a.elapsed_time(b) for a, b in cm]))
+        per_call["route_coupled"] = [a.elapsed_time(b) for a, b in cm]
+        coupled_ms = float(np.mean(per_call["route_coupled"]))
 
     # the whole update of one residual site (e.g. the FFN site): PAR of the skipped
     # frames with every anchor's own update fused in, timed on its own
@@ -303,7 +309,8 @@ def main():
                                       stream=stream)
             bm[i][1].record(stream)
         torch.cuda.synchronize()
-        block_ms = float(np.mean([a.elapsed_time(b) for a, b in bm]))
+        per_call["par_block_update"] = [a.elapsed_time(b) for a, b in bm]
+        block_ms = float(np.mean(per_call["par_block_update"]))
 
     # control-aware frame selection for the next block (both control branches, bf16),
     # timed on its own
@@ -327,7 +334,8 @@ def main():
                                    workspace=sel_ws, stream=stream)
             sm[i][1].record(stream)
         torch.cuda.synchronize()
-        sel_ms = float(np.mean([a.elapsed_time(b) for a, b in sm]))
+        per_call["frame_select"] = [a.elapsed_time(b) for a, b in sm]
+        sel_ms = float(np.mean(per_call["frame_select"]))
         del ctl
 
     # spectral diagnostics of the skipped frames (validation, not inference): error
@@ -364,10 +372,12 @@ def main():
         "config": {"workload": w.name, "frames": w.n_frames, "grid": f"{w.Hg}x{w.Wg}",
                    "D": w.D, "heads": w.H, "dh": w.dh, "anchors": list(w.anchors),
                    "history_chunks": w.M, "chunk_tokens": w.Bv, "topk": w.topk,
-                   "par_mode": "accumulate", "input_copies": N_COPIES},
+                   "par_mode": "accumulate", "input_copies": N_COPIES,
+                   "attn_input_seeds": seeds if w.has_attention else None},
         "per_call_ms": {"route": route_ms, "attn": attn_ms, "par": par_ms,
                         "route_coupled": coupled_ms, "par_block_update": block_ms,
                         "frame_select": sel_ms, "spectral_diagnostics": diag_ms},
+        "per_call_ms_median": {c: float(np.median(v)) for c, v in per_call.items()},
     }
     extra = {}
     traffic = load_traffic(w.name)
