@@ -2,32 +2,63 @@
 // eq:bandenergy, eq:phaseerror; the relative error e_t of Sec. 3.1
 // eq:sensitivity), with PAR's tile and FFT conventions (App. A.2).
 //
-// diag_tile   grid (tile, channel block of 64, frame); frames that are anchors
-//             exit.  Each lane owns one channel of one tile of the skipped frame t
-//             and transforms (orthonormal real 2-D DFT, any tile size up to 8x8,
-//             runtime loops over per-lane LDS columns) the reference R_t, the
-//             reconstruction R_hat_t and the two anchors of t's pair.  It adds up
-//             kappa |F_t - F_hat_t|^2 per radial band, kappa |F_t|^2, and the
-//             energy-weighted circular distance of the transport phase; it writes
+// diag_tile   grid (tile, channel block of 256, frame); frames that are anchors
+//             exit.  Each thread owns one channel of one tile of the skipped frame
+//             t and transforms (orthonormal real 2-D DFT) the reference R_t, the
+//             reconstruction R_hat_t, the anchor a of t's pair and the linear
+//             interpolation (1 - alpha) R_a + alpha R_b.  It adds up
+//             kappa |F_t - F_hat_t|^2 per radial band, kappa |F_t|^2 and the
+//             energy-weighted circular distance of the transport phase, and writes
 //             the oracle corrections of the linear interpolation
 //             (|F_lin| e^{i Arg F_t} and |F_t| e^{i Arg F_lin}, inverted) when
-//             asked.  The 64 lanes are summed by a butterfly into one partial per
-//             (frame, tile, channel block).
-// diag_final  one block per frame: the partials in fixed order (fp64), then e_t,
+//             asked.  The block sums its 256 threads in a fixed order into one
+//             partial per (frame, tile, channel block).
+// diag_final  one wave per frame: the partials in fixed order (fp64), then e_t,
 //             the band fractions and the phase error.
-// Not a hot path: clarity over speed (runtime tile sizes, spectra in LDS).
+//
+// The tile edges are runtime values (1..8; edge tiles are smaller), the same for
+// every thread of a block.  Each transform is a matrix DFT over the largest tile,
+// held in registers, with zero rows and columns past the tile; its twiddles come
+// from a constant table indexed by the (uniform) edge length, so they are scalar
+// operands.  At most two spectra are live at once.
 #include "cast_common.h"
+#include "fft_tile.h"
 
 namespace cast {
 
 namespace {
 
-constexpr int kLanes = 64;
+constexpr int kDiagThreads = 256;
 constexpr int kT = kParMaxTile;            // largest tile edge
-constexpr int kNkx = kT / 2 + 1;
-constexpr int kSpec = kT * kNkx;           // stored bins of the largest tile
+constexpr int kNkx = kT / 2 + 1;           // stored columns of the largest tile
+constexpr int kBins = kT * kNkx;
 constexpr int kVals = kDiagMaxBands + 3;   // band energies, |F_t|^2, phase sum, weight sum
 constexpr float kPi = 3.14159265358979323846f;
+
+// cos and sin of 2 pi (k j mod n) / n for n = 1 .. 8 and k, j < 8, rounded from
+// double, with the quarter turns exact (so the self-conjugate bins of a real
+// tile come out exactly real); entries with k or j >= n meet zero data or give
+// bins that are not used.
+struct TwTable {
+  float c[kT + 1][kT][kT];
+  float s[kT + 1][kT][kT];
+  constexpr TwTable() : c(), s() {
+    for (int n = 1; n <= kT; ++n)
+      for (int k = 0; k < kT; ++k)
+        for (int j = 0; j < kT; ++j) {
+          const int m = (k * j) % n;
+          if (4 * m % n == 0) {   // m n / 4 turns: 0, 1/4, 1/2, 3/4
+            const int q = 4 * m / n;
+            c[n][k][j] = q == 0 ? 1.0f : (q == 2 ? -1.0f : 0.0f);
+            s[n][k][j] = q == 1 ? 1.0f : (q == 3 ? -1.0f : 0.0f);
+          } else {
+            c[n][k][j] = (float)fft::tw_cos(m, n);
+            s[n][k][j] = (float)fft::tw_sin(m, n);
+          }
+        }
+  }
+};
+__constant__ TwTable kTw = TwTable();
 
 struct DiagArgs {
   const float* ref;
@@ -43,97 +74,100 @@ struct DiagArgs {
   short anchors[kParMaxAnchors];
 };
 
-// Per-lane LDS storage: element k of lane l at [k * 64 + l] (conflict-free).
-struct Spec {
-  float* re;
-  float* im;
-  __device__ float& r(int k) { return re[k * kLanes + threadIdx.x]; }
-  __device__ float& i(int k) { return im[k * kLanes + threadIdx.x]; }
-};
+using Spec = float[kT][kNkx];
+using Row = float[kT];
 
-// twiddles e^{-2 pi i j / n} for n = 1 .. 8: c[n][j], s[n][j] = cos, sin of 2 pi j / n
-struct Tw {
-  float c[kT + 1][kT];
-  float s[kT + 1][kT];
-};
-
-__device__ void load_tile(const float* frame, const DiagArgs& a, int y0, int x0, int hp, int wp,
-                          int c, float* x) {
-  for (int y = 0; y < hp; ++y)
-    for (int xx = 0; xx < wp; ++xx)
-      x[(y * wp + xx) * kLanes + threadIdx.x] = frame[((long long)(y0 + y) * a.Wg + x0 + xx) * a.D + c];
-}
-
-// Orthonormal forward real 2-D DFT of the lane's tile values x[hp][wp] into F
-// (bins ky in [0, hp), kx in [0, wp/2], slot ky * kNkx + kx); t holds the rows.
-__device__ void fwd(const float* x, int hp, int wp, const Tw& tw, Spec t, Spec F) {
-  const int nkx = wp / 2 + 1;
-  for (int y = 0; y < hp; ++y)
-    for (int kx = 0; kx < nkx; ++kx) {
-      float re = 0.0f, im = 0.0f;
-      for (int xx = 0; xx < wp; ++xx) {
-        const float v = x[(y * wp + xx) * kLanes + threadIdx.x];
-        const int j = (kx * xx) % wp;
-        re = fmaf(v, tw.c[wp][j], re);
-        im = fmaf(-v, tw.s[wp][j], im);
-      }
-      t.r(y * kNkx + kx) = re;
-      t.i(y * kNkx + kx) = im;
+// Orthonormal forward real 2-D DFT of a tile whose row y (zero past wp) is
+// produced by row(y, v); rows y >= hp are zero.  Bins ky < hp, kx <= wp/2 of
+// (Fr, Fi) are the transform; the others hold finite values of no meaning.
+template <class RowFn>
+__device__ __forceinline__ void fwd2(RowFn&& row, int hp, int wp, Spec& Fr, Spec& Fi) {
+#pragma unroll
+  for (int y = 0; y < kT; ++y) {
+    Row v;
+    if (y < hp) {
+      row(y, v);
+    } else {
+#pragma unroll
+      for (int x = 0; x < kT; ++x) v[x] = 0.0f;
     }
+#pragma unroll
+    for (int kx = 0; kx < kNkx; ++kx) {
+      float re = 0.0f, im = 0.0f;
+#pragma unroll
+      for (int x = 0; x < kT; ++x) {
+        re = fmaf(v[x], kTw.c[wp][kx][x], re);
+        im = fmaf(-v[x], kTw.s[wp][kx][x], im);
+      }
+      Fr[y][kx] = re;
+      Fi[y][kx] = im;
+    }
+  }
   const float sc = 1.0f / sqrtf((float)(hp * wp));
-  for (int kx = 0; kx < nkx; ++kx)
-    for (int ky = 0; ky < hp; ++ky) {
+#pragma unroll
+  for (int kx = 0; kx < kNkx; ++kx) {
+    Row cr, ci;
+#pragma unroll
+    for (int y = 0; y < kT; ++y) { cr[y] = Fr[y][kx]; ci[y] = Fi[y][kx]; }
+#pragma unroll
+    for (int ky = 0; ky < kT; ++ky) {
       float re = 0.0f, im = 0.0f;
-      for (int y = 0; y < hp; ++y) {
-        const int j = (ky * y) % hp;
-        const float cr = t.r(y * kNkx + kx), ci = t.i(y * kNkx + kx);
-        const float c = tw.c[hp][j], s = tw.s[hp][j];   // e^{-i phi} = c - i s
-        re += cr * c + ci * s;
-        im += ci * c - cr * s;
+#pragma unroll
+      for (int y = 0; y < kT; ++y) {   // (cr + i ci)(c - i s)
+        const float c = kTw.c[hp][ky][y], s = kTw.s[hp][ky][y];
+        re = fmaf(cr[y], c, fmaf(ci[y], s, re));
+        im = fmaf(ci[y], c, fmaf(-cr[y], s, im));
       }
-      F.r(ky * kNkx + kx) = re * sc;
-      F.i(ky * kNkx + kx) = im * sc;
+      Fr[ky][kx] = re * sc;
+      Fi[ky][kx] = im * sc;
     }
+  }
 }
 
-// Inverse: x[y][x] = (hp wp)^-1/2 sum_{stored bins} kappa Re(F e^{+i phi}), the real
-// inverse of the Hermitian spectrum; t holds the column pass.
-__device__ void inv(Spec F, int hp, int wp, const Tw& tw, Spec t, float* x) {
+// Inverse of the Hermitian spectrum given by its stored bins (zero outside the
+// tile's bins): x[y][x] = (hp wp)^-1/2 sum_{stored} kappa Re(F e^{+i phi}).  The
+// column pass runs in place; each output row y < hp goes to out(y, v).
+template <class OutFn>
+__device__ __forceinline__ void inv2(Spec& Fr, Spec& Fi, int hp, int wp, OutFn&& out) {
+#pragma unroll
+  for (int kx = 0; kx < kNkx; ++kx) {
+    Row cr, ci;
+#pragma unroll
+    for (int ky = 0; ky < kT; ++ky) { cr[ky] = Fr[ky][kx]; ci[ky] = Fi[ky][kx]; }
+#pragma unroll
+    for (int y = 0; y < kT; ++y) {
+      float re = 0.0f, im = 0.0f;
+#pragma unroll
+      for (int ky = 0; ky < kT; ++ky) {   // (cr + i ci)(c + i s)
+        const float c = kTw.c[hp][ky][y], s = kTw.s[hp][ky][y];
+        re = fmaf(cr[ky], c, fmaf(-ci[ky], s, re));
+        im = fmaf(ci[ky], c, fmaf(cr[ky], s, im));
+      }
+      Fr[y][kx] = re;
+      Fi[y][kx] = im;
+    }
+  }
   const int nkx = wp / 2 + 1;
-  for (int kx = 0; kx < nkx; ++kx)
-    for (int y = 0; y < hp; ++y) {
-      float re = 0.0f, im = 0.0f;
-      for (int ky = 0; ky < hp; ++ky) {
-        const int j = (ky * y) % hp;
-        const float fr = F.r(ky * kNkx + kx), fi = F.i(ky * kNkx + kx);
-        const float c = tw.c[hp][j], s = tw.s[hp][j];   // e^{+i phi} = c + i s
-        re += fr * c - fi * s;
-        im += fi * c + fr * s;
-      }
-      t.r(y * kNkx + kx) = re;
-      t.i(y * kNkx + kx) = im;
-    }
   const float sc = 1.0f / sqrtf((float)(hp * wp));
-  for (int y = 0; y < hp; ++y)
-    for (int xx = 0; xx < wp; ++xx) {
-      float v = 0.0f;
-      for (int kx = 0; kx < nkx; ++kx) {
-        const int j = (kx * xx) % wp;
-        const float kap = (kx == 0 || 2 * kx == wp) ? 1.0f : 2.0f;
-        v += kap * (t.r(y * kNkx + kx) * tw.c[wp][j] - t.i(y * kNkx + kx) * tw.s[wp][j]);
+#pragma unroll
+  for (int y = 0; y < kT; ++y) {
+    if (y >= hp) continue;
+    Row v;
+#pragma unroll
+    for (int x = 0; x < kT; ++x) {
+      float acc = 0.0f;
+#pragma unroll
+      for (int kx = 0; kx < kNkx; ++kx) {
+        const float kap = kx >= nkx ? 0.0f : ((kx == 0 || 2 * kx == wp) ? 1.0f : 2.0f);
+        acc = fmaf(kap, fmaf(Fr[y][kx], kTw.c[wp][kx][x], -Fi[y][kx] * kTw.s[wp][kx][x]), acc);
       }
-      x[(y * wp + xx) * kLanes + threadIdx.x] = v * sc;
+      v[x] = acc * sc;
     }
+    out(y, v);
+  }
 }
 
-__device__ void store_tile(float* frame, const DiagArgs& a, int y0, int x0, int hp, int wp, int c,
-                           const float* x) {
-  for (int y = 0; y < hp; ++y)
-    for (int xx = 0; xx < wp; ++xx)
-      frame[((long long)(y0 + y) * a.Wg + x0 + xx) * a.D + c] = x[(y * wp + xx) * kLanes + threadIdx.x];
-}
-
-__global__ __launch_bounds__(kLanes) void diag_tile_kernel(DiagArgs a) {
+__global__ __launch_bounds__(kDiagThreads) void diag_tile_kernel(DiagArgs a) {
   const int tile = blockIdx.x, chb = blockIdx.y, t = blockIdx.z;
   // the pair of frame t (eq:block), or nothing for an anchor
   int j = 0;
@@ -143,114 +177,154 @@ __global__ __launch_bounds__(kLanes) void diag_tile_kernel(DiagArgs a) {
   const int fa = a.anchors[pr], fb = a.anchors[pr + 1];
   const float alpha = (float)(t - fa) / (float)(fb - fa);
 
-  __shared__ Tw tw;
-  __shared__ float xs[kT * kT * kLanes];
-  __shared__ float s_re[4][kSpec * kLanes], s_im[4][kSpec * kLanes];
-  const int lane = threadIdx.x;
-  for (int k = lane; k < (kT + 1) * kT; k += kLanes) {
-    const int n = k / kT, jj = k % kT;
-    float sn = 0.0f, cs = 1.0f;
-    if (n > 0) sincospif(2.0f * (float)jj / (float)n, &sn, &cs);
-    tw.c[n][jj] = cs;
-    tw.s[n][jj] = sn;
-  }
-  __syncthreads();
-  Spec Ft{s_re[0], s_im[0]}, Fo{s_re[1], s_im[1]}, Fl{s_re[2], s_im[2]}, T{s_re[3], s_im[3]};
-
   const int ty = tile / a.n_tx, tx = tile - (tile / a.n_tx) * a.n_tx;
   const int y0 = ty * a.tile_h, x0 = tx * a.tile_w;
   const int hp = min(a.tile_h, a.Hg - y0), wp = min(a.tile_w, a.Wg - x0), nkx = wp / 2 + 1;
-  const int c_raw = chb * kLanes + lane;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+  // per-bin weights of the tile (bin b = ky * kNkx + kx): kappa (0 outside the
+  // tile's stored bins), and kappa times the indicator of each radial band
+  __shared__ float s_kap[kBins];
+  __shared__ float s_w[kDiagMaxBands][kBins];
+  __shared__ float s_red[kDiagThreads / 64][kVals];
+  if (tid < kBins) {
+    const int ky = tid / kNkx, kx = tid - (tid / kNkx) * kNkx;
+    const bool valid = ky < hp && kx < nkx;
+    const float kap = valid ? ((kx == 0 || 2 * kx == wp) ? 1.0f : 2.0f) : 0.0f;
+    // maximum physical radius of the tile's stored bins (for nu)
+    double rmax = 0.0;
+    for (int y = 0; y < hp; ++y)
+      for (int x = 0; x < nkx; ++x) {
+        const int ys = 2 * y <= hp ? y : y - hp;
+        rmax = fmax(rmax, sqrt((double)ys * ys / ((double)hp * hp) + (double)x * x / ((double)wp * wp)));
+      }
+    const int kys = 2 * ky <= hp ? ky : ky - hp;
+    const double nu = rmax > 0.0 ? sqrt((double)kys * kys / ((double)hp * hp) +
+                                        (double)kx * kx / ((double)wp * wp)) / rmax : 0.0;
+    int band = 0;
+    while (band + 1 < a.n_bands && nu >= a.edges[band + 1]) ++band;
+    s_kap[tid] = kap;
+    for (int v = 0; v < kDiagMaxBands; ++v) s_w[v][tid] = v == band ? kap : 0.0f;
+  }
+  __syncthreads();
+
+  // the lambdas below capture locals only (capturing the kernel argument by
+  // reference would copy it to private memory)
+  const float* const ref = a.ref;
+  const float* const approx = a.approx;
+  float* const r_phase = a.r_phase;
+  float* const r_mag = a.r_mag;
+  const long long frame_elems = a.frame_elems, Wg = a.Wg, D = a.D;
+  const int c_raw = chb * kDiagThreads + tid;
   const bool live = c_raw < a.D;
   const int c = live ? c_raw : a.D - 1;
-  const float* ref = a.ref;
-  // maximum physical radius of the tile's stored bins (for nu)
-  double rmax = 0.0;
-  for (int ky = 0; ky < hp; ++ky)
-    for (int kx = 0; kx < nkx; ++kx) {
-      const int kys = 2 * ky <= hp ? ky : ky - hp;
-      rmax = fmax(rmax, sqrt((double)kys * kys / ((double)hp * hp) + (double)kx * kx / ((double)wp * wp)));
-    }
+  // element offset of (y, x) of the tile in frame f, channel c
+  auto off = [=](int f, int y, int x) -> long long {
+    return (long long)f * frame_elems + ((long long)(y0 + y) * Wg + (x0 + x)) * D + c;
+  };
+  auto load_row = [=](const float* base, int f, int y, Row& v) {
+#pragma unroll
+    for (int x = 0; x < kT; ++x) v[x] = x < wp ? __builtin_nontemporal_load(base + off(f, y, x)) : 0.0f;
+  };
 
   float acc[kVals];
+#pragma unroll
   for (int v = 0; v < kVals; ++v) acc[v] = 0.0f;
-  // reference and reconstruction: band energies of the error, reference energy
-  load_tile(ref + (long long)t * a.frame_elems, a, y0, x0, hp, wp, c, xs);
-  fwd(xs, hp, wp, tw, T, Ft);
-  load_tile(a.approx + (long long)t * a.frame_elems, a, y0, x0, hp, wp, c, xs);
-  fwd(xs, hp, wp, tw, T, Fo);
-  for (int ky = 0; ky < hp; ++ky)
-    for (int kx = 0; kx < nkx; ++kx) {
+
+  // F_t, and the error spectrum F_t - F_hat_t: band energies, reference energy
+  Spec Tr, Ti, Or, Oi;
+  fwd2([&](int y, Row& v) { load_row(ref, t, y, v); }, hp, wp, Tr, Ti);
+  fwd2([&](int y, Row& v) { load_row(approx, t, y, v); }, hp, wp, Or, Oi);
+#pragma unroll
+  for (int ky = 0; ky < kT; ++ky)
+#pragma unroll
+    for (int kx = 0; kx < kNkx; ++kx) {
       const int b = ky * kNkx + kx;
-      const float kap = (kx == 0 || 2 * kx == wp) ? 1.0f : 2.0f;
-      const float dr = Ft.r(b) - Fo.r(b), di = Ft.i(b) - Fo.i(b);
-      const int kys = 2 * ky <= hp ? ky : ky - hp;
-      const double nu = rmax > 0.0 ? sqrt((double)kys * kys / ((double)hp * hp) +
-                                          (double)kx * kx / ((double)wp * wp)) / rmax : 0.0;
-      int band = 0;
-      while (band + 1 < a.n_bands && nu >= a.edges[band + 1]) ++band;
-      acc[band] += kap * (dr * dr + di * di);
-      acc[kDiagMaxBands] += kap * (Ft.r(b) * Ft.r(b) + Ft.i(b) * Ft.i(b));
+      const float dr = Tr[ky][kx] - Or[ky][kx], di = Ti[ky][kx] - Oi[ky][kx];
+      const float e = fmaf(dr, dr, di * di);
+#pragma unroll
+      for (int v = 0; v < kDiagMaxBands; ++v) acc[v] = fmaf(s_w[v][b], e, acc[v]);
+      acc[kDiagMaxBands] = fmaf(s_kap[b], fmaf(Tr[ky][kx], Tr[ky][kx], Ti[ky][kx] * Ti[ky][kx]),
+                                acc[kDiagMaxBands]);
     }
-  // anchor a: transport phase error; F_lin = (1 - alpha) F_a + alpha F_b
-  const bool want_corr = a.r_phase != nullptr || a.r_mag != nullptr;
-  if (a.theta != nullptr || want_corr) {
-    load_tile(ref + (long long)fa * a.frame_elems, a, y0, x0, hp, wp, c, xs);
-    fwd(xs, hp, wp, tw, T, Fo);
+
+  // anchor a: transport phase error against theta
+  if (a.theta != nullptr) {
+    fwd2([&](int y, Row& v) { load_row(ref, fa, y, v); }, hp, wp, Or, Oi);
     const int nkx_out = a.tile_w / 2 + 1;
-    for (int ky = 0; ky < hp; ++ky)
-      for (int kx = 0; kx < nkx; ++kx) {
-        const int b = ky * kNkx + kx;
-        Fl.r(b) = (1.0f - alpha) * Fo.r(b);
-        Fl.i(b) = (1.0f - alpha) * Fo.i(b);
-        if (a.theta == nullptr) continue;
-        const float th = a.theta[((long long)pr * a.n_tiles + tile) * (a.tile_h * nkx_out) + ky * nkx_out + kx];
-        const float at2 = Ft.r(b) * Ft.r(b) + Ft.i(b) * Ft.i(b);
-        const float aa2 = Fo.r(b) * Fo.r(b) + Fo.i(b) * Fo.i(b);
+    const float* th_tile = a.theta + ((long long)pr * a.n_tiles + tile) * (a.tile_h * nkx_out);
+#pragma unroll
+    for (int ky = 0; ky < kT; ++ky)
+#pragma unroll
+      for (int kx = 0; kx < kNkx; ++kx) {
+        if (ky >= hp || kx >= nkx) continue;   // uniform: bins of the tile only
+        const float th = th_tile[ky * nkx_out + kx];
+        const float at2 = fmaf(Tr[ky][kx], Tr[ky][kx], Ti[ky][kx] * Ti[ky][kx]);
+        const float aa2 = fmaf(Or[ky][kx], Or[ky][kx], Oi[ky][kx] * Oi[ky][kx]);
         if (at2 > 0.0f && aa2 > 0.0f) {
-          const float kap = (kx == 0 || 2 * kx == wp) ? 1.0f : 2.0f;
-          const float w = kap * at2;
-          float x = atan2f(Ft.i(b), Ft.r(b)) - atan2f(Fo.i(b), Fo.r(b)) - alpha * th;
+          const float w = s_kap[ky * kNkx + kx] * at2;
+          float x = atan2f(Ti[ky][kx], Tr[ky][kx]) - atan2f(Oi[ky][kx], Or[ky][kx]) - alpha * th;
           x = x - 2.0f * kPi * floorf((x + kPi) / (2.0f * kPi));
-          acc[kDiagMaxBands + 1] += w * fabsf(x);
+          acc[kDiagMaxBands + 1] = fmaf(w, fabsf(x), acc[kDiagMaxBands + 1]);
           acc[kDiagMaxBands + 2] += w;
         }
       }
   }
-  if (want_corr) {
-    load_tile(ref + (long long)fb * a.frame_elems, a, y0, x0, hp, wp, c, xs);
-    fwd(xs, hp, wp, tw, T, Fo);
-    for (int ky = 0; ky < hp; ++ky)
-      for (int kx = 0; kx < nkx; ++kx) {
-        const int b = ky * kNkx + kx;
-        Fl.r(b) += alpha * Fo.r(b);
-        Fl.i(b) += alpha * Fo.i(b);
+
+  // oracle corrections of the linear interpolation F_lin, the transform of
+  // (1 - alpha) R_a + alpha R_b
+  if (r_phase != nullptr || r_mag != nullptr) {
+    fwd2([&](int y, Row& v) {
+      Row vb;
+      load_row(ref, fa, y, v);
+      load_row(ref, fb, y, vb);
+#pragma unroll
+      for (int x = 0; x < kT; ++x) v[x] = (1.0f - alpha) * v[x] + alpha * vb[x];
+    }, hp, wp, Or, Oi);
+    // in place: T <- |F_lin| e^{i Arg F_t}, O <- |F_t| e^{i Arg F_lin} (a vanishing
+    // spectrum gives phase factor 1); bins outside the tile are zeroed
+#pragma unroll
+    for (int ky = 0; ky < kT; ++ky)
+#pragma unroll
+      for (int kx = 0; kx < kNkx; ++kx) {
+        const bool valid = ky < hp && kx < nkx;
+        const float mt = sqrtf(fmaf(Tr[ky][kx], Tr[ky][kx], Ti[ky][kx] * Ti[ky][kx]));
+        const float ml = sqrtf(fmaf(Or[ky][kx], Or[ky][kx], Oi[ky][kx] * Oi[ky][kx]));
+        const float p_re = mt > 0.0f ? ml * (Tr[ky][kx] / mt) : ml;
+        const float p_im = mt > 0.0f ? ml * (Ti[ky][kx] / mt) : 0.0f;
+        const float m_re = ml > 0.0f ? mt * (Or[ky][kx] / ml) : mt;
+        const float m_im = ml > 0.0f ? mt * (Oi[ky][kx] / ml) : 0.0f;
+        Tr[ky][kx] = valid ? p_re : 0.0f;
+        Ti[ky][kx] = valid ? p_im : 0.0f;
+        Or[ky][kx] = valid ? m_re : 0.0f;
+        Oi[ky][kx] = valid ? m_im : 0.0f;
       }
-    for (int which = 0; which < 2; ++which) {
-      float* dst = which == 0 ? a.r_phase : a.r_mag;
-      if (dst == nullptr) continue;
-      for (int ky = 0; ky < hp; ++ky)
-        for (int kx = 0; kx < nkx; ++kx) {
-          const int b = ky * kNkx + kx;
-          const float mt = sqrtf(Ft.r(b) * Ft.r(b) + Ft.i(b) * Ft.i(b));
-          const float ml = sqrtf(Fl.r(b) * Fl.r(b) + Fl.i(b) * Fl.i(b));
-          // modulus of one spectrum, unit phase factor of the other (1 where it vanishes)
-          const float m = which == 0 ? ml : mt;
-          const float pr_ = which == 0 ? Ft.r(b) : Fl.r(b), pi_ = which == 0 ? Ft.i(b) : Fl.i(b);
-          const float pm = which == 0 ? mt : ml;
-          Fo.r(b) = pm > 0.0f ? m * (pr_ / pm) : m;
-          Fo.i(b) = pm > 0.0f ? m * (pi_ / pm) : 0.0f;
-        }
-      inv(Fo, hp, wp, tw, T, xs);
-      if (live) store_tile(dst + (long long)t * a.frame_elems, a, y0, x0, hp, wp, c, xs);
-    }
+    if (r_phase != nullptr)
+      inv2(Tr, Ti, hp, wp, [=](int y, const Row& v) {
+#pragma unroll
+        for (int x = 0; x < kT; ++x)
+          if (live && x < wp) r_phase[off(t, y, x)] = v[x];
+      });
+    if (r_mag != nullptr)
+      inv2(Or, Oi, hp, wp, [=](int y, const Row& v) {
+#pragma unroll
+        for (int x = 0; x < kT; ++x)
+          if (live && x < wp) r_mag[off(t, y, x)] = v[x];
+      });
   }
-  // lanes past D add nothing; then the 64 lanes in butterfly order
+
+  // threads past D add nothing; then the block's 256 threads in a fixed order
+#pragma unroll
   for (int v = 0; v < kVals; ++v) {
     float s = live ? acc[v] : 0.0f;
     for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
-    if (lane == 0)
-      a.partial[(((long long)t * a.n_tiles + tile) * a.n_chblk + chb) * kVals + v] = s;
+    if (lane == 0) s_red[wave][v] = s;
+  }
+  __syncthreads();
+  if (tid < kVals) {
+    float s = 0.0f;
+    for (int w = 0; w < kDiagThreads / 64; ++w) s += s_red[w][tid];
+    a.partial[(((long long)t * a.n_tiles + tile) * a.n_chblk + chb) * kVals + tid] = s;
   }
 }
 
@@ -266,14 +340,14 @@ struct FinalArgs {
   int n_anchor;
 };
 
-__global__ __launch_bounds__(kLanes) void diag_final_kernel(FinalArgs a) {
+__global__ __launch_bounds__(64) void diag_final_kernel(FinalArgs a) {
   const int t = blockIdx.x, lane = threadIdx.x;
   bool is_anchor = false;
   for (int j = 0; j < a.n_anchor; ++j) is_anchor |= a.anchors[j] == t;
   double s[kVals];
   for (int v = 0; v < kVals; ++v) s[v] = 0.0;
   if (!is_anchor)
-    for (int it = lane; it < a.n_items; it += kLanes)
+    for (int it = lane; it < a.n_items; it += 64)
       for (int v = 0; v < kVals; ++v) s[v] += (double)a.partial[((long long)t * a.n_items + it) * kVals + v];
   for (int v = 0; v < kVals; ++v)
     for (int o = 32; o > 0; o >>= 1) s[v] += __shfl_xor(s[v], o);
@@ -293,7 +367,7 @@ __global__ __launch_bounds__(kLanes) void diag_final_kernel(FinalArgs a) {
 
 size_t diag_workspace_bytes(int n_frames, int Hg, int Wg, int D, int tile_h, int tile_w) {
   const long long tiles = (long long)((Hg + tile_h - 1) / tile_h) * ((Wg + tile_w - 1) / tile_w);
-  const long long chblk = (D + kLanes - 1) / kLanes;
+  const long long chblk = (D + kDiagThreads - 1) / kDiagThreads;
   return align_up((size_t)(n_frames * tiles * chblk * kVals) * sizeof(float));
 }
 
@@ -317,14 +391,15 @@ cast_status_t launch_diag(const float* ref, const float* approx, const float* th
   a.tile_w = p.tile_w;
   a.n_tx = (Wg + p.tile_w - 1) / p.tile_w;
   a.n_tiles = a.n_tx * ((Hg + p.tile_h - 1) / p.tile_h);
-  a.n_chblk = (D + kLanes - 1) / kLanes;
+  a.n_chblk = (D + kDiagThreads - 1) / kDiagThreads;
   a.n_anchor = n_anchor;
   a.n_frames = n_frames;
   a.n_bands = p.n_bands;
   a.eps = p.eps;
   for (int k = 0; k <= p.n_bands; ++k) a.edges[k] = (double)p.band_edges[k];
   for (int j = 0; j < n_anchor; ++j) a.anchors[j] = (short)anchors[j];
-  hipLaunchKernelGGL(diag_tile_kernel, dim3(a.n_tiles, a.n_chblk, n_frames), dim3(kLanes), 0, stream, a);
+  hipLaunchKernelGGL(diag_tile_kernel, dim3(a.n_tiles, a.n_chblk, n_frames), dim3(kDiagThreads), 0,
+                     stream, a);
   cast_status_t st = check_launch("diag_tile");
   if (st != CAST_OK) return st;
   FinalArgs f{};
@@ -337,7 +412,7 @@ cast_status_t launch_diag(const float* ref, const float* approx, const float* th
   f.eps = p.eps;
   for (int j = 0; j < n_anchor; ++j) f.anchors[j] = (short)anchors[j];
   f.n_anchor = n_anchor;
-  hipLaunchKernelGGL(diag_final_kernel, dim3(n_frames), dim3(kLanes), 0, stream, f);
+  hipLaunchKernelGGL(diag_final_kernel, dim3(n_frames), dim3(64), 0, stream, f);
   return check_launch("diag_final");
 }
 
