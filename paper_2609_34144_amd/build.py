@@ -39,6 +39,10 @@ UNITS = [("par.hip", "par", ["-fno-signed-zeros"])] + [
     ("route_coupled.hip", "route_coupled", []),
     ("frame_select.hip", "frame_select", []),
     ("diag.hip", "diag", []),
+] + [
+    ("diag_fixed.hip", f"diag_fixed_{hp}", ["-fno-signed-zeros", f"-DCAST_DIAG_HP={hp}"])
+    for hp in range(8, 0, -1)
+] + [
     ("capi.hip", "capi", []),
 ]
 
