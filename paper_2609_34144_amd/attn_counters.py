@@ -70,7 +70,8 @@ def summarize(workload: str, db: str, cmd: str, out_stem: str) -> dict:
         "issued / algorithmic": v["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512 / algo,
         "VALU instructions per MFMA": v["SQ_INSTS_VALU"] / v["SQ_INSTS_MFMA"],
         "transcendental per MFMA": v["SQ_INSTS_VALU_TRANS_F32"] / v["SQ_INSTS_MFMA"],
-        "VALU active % (per SIMD)": 100.0 * v["SQ_ACTIVE_INST_VALU"] / (cyc * N_SIMD),
+        # SQ_ACTIVE_INST_VALU counts quad-cycles
+        "VALU active % (per SIMD)": 100.0 * 4.0 * v["SQ_ACTIVE_INST_VALU"] / (cyc * N_SIMD),
         "LDS bank conflicts per MFMA": v["SQ_LDS_BANK_CONFLICT"] / v["SQ_INSTS_MFMA"],
     }
     with open(out_stem + ".md", "w") as fh:
@@ -84,6 +85,7 @@ def summarize(workload: str, db: str, cmd: str, out_stem: str) -> dict:
         for k, x in d.items():
             fh.write(f"| {k} | {x:.4g} |\n")
         fh.write(f"\nMFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / {N_XCD} x {N_SIMD} SIMDs); "
+                 f"VALU active = 4 SQ_ACTIVE_INST_VALU (quad-cycles) / (GRBM_GUI_ACTIVE / {N_XCD} x {N_SIMD}); "
                  f"clock = GRBM_GUI_ACTIVE / {N_XCD} / duration; issued FLOPs = "
                  "SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512.\n")
     return d
