@@ -24,6 +24,7 @@ namespace {
 constexpr int kOmM = 16;          // blocks per omission workgroup (4 per wave)
 constexpr int kThreads = 256;
 constexpr int kRefineThreads = 64;   // the solver runs in one wave per head
+constexpr int kRefineCacheU = 8192;  // u of one head (n_a * M floats) staged in LDS up to this
 
 struct CoupledArgs {
   const float* means_qk;   // [n_a + M, D]: q_bar rows, then k_bar rows
@@ -205,6 +206,7 @@ struct Coeffs {
 
 // One wave per head: the solver is a chain of small sorts and sums, and with a
 // single wave every barrier is immediate and every sum a shuffle butterfly.
+template <bool CACHE_U>
 __global__ __launch_bounds__(kRefineThreads) void coupled_refine_kernel(CoupledArgs a) {
   extern __shared__ unsigned long long keys[];        // [P]
   const int M = a.M, n_a = a.n_a, k = a.k_eff, h = blockIdx.x;
@@ -212,11 +214,21 @@ __global__ __launch_bounds__(kRefineThreads) void coupled_refine_kernel(CoupledA
   while (P < M) P <<= 1;
   float* g = reinterpret_cast<float*>(keys + P);      // [M] gains of the visited row
   uint32_t* xm = reinterpret_cast<uint32_t*>(g + M);  // [n_a * M] retain bits
+  const int nwords = (n_a * M + 31) / 32;
+  float* su = reinterpret_cast<float*>(xm + nwords);  // [n_a * M] u of this head (CACHE_U)
   __shared__ Coeffs cf;
   __shared__ float pair_ab[kCoupledMaxAnchors], pair_c[kCoupledMaxAnchors];
   const int tid = threadIdx.x;
-  const int nwords = (n_a * M + 31) / 32;
-  auto U = [&](int i, int m) -> float { return a.u[((long long)i * a.H + h) * M + m]; };
+  // u is read at every step of the solver: staged in LDS when it fits
+  if constexpr (CACHE_U)
+    for (int x = tid; x < n_a * M; x += kRefineThreads) {
+      const int i = x / M, m = x - (x / M) * M;
+      su[x] = a.u[((long long)i * a.H + h) * M + m];
+    }
+  auto U = [&](int i, int m) -> float {
+    if constexpr (CACHE_U) return su[i * M + m];
+    else return a.u[((long long)i * a.H + h) * M + m];
+  };
   auto X = [&](int i, int m) -> float {
     const int bit = i * M + m;
     return (xm[bit >> 5] >> (bit & 31)) & 1u ? 1.0f : 0.0f;
@@ -256,6 +268,18 @@ __global__ __launch_bounds__(kRefineThreads) void coupled_refine_kernel(CoupledA
   // TopK of the values in g[0..M): leaves the winners first in keys[], returns
   // their sum (the same on every thread)
   auto topk_sum = [&]() -> float {
+    if (M <= kRefineThreads) {
+      // one value per lane: its rank is the number of larger keys (the keys are
+      // distinct, so the ranks are too); the winners are stored in rank order
+      const bool in = tid < M;
+      const float gv = in ? g[tid] : 0.0f;
+      const unsigned long long km = in ? order_key(gv, tid) : 0ull;
+      int rank = 0;
+      for (int j = 0; j < M; ++j) rank += __shfl(km, j) > km ? 1 : 0;
+      const bool win = in && rank < k;
+      if (win) keys[rank] = km;
+      return wave_sum(win ? gv : 0.0f);
+    }
     for (int m = tid; m < P; m += kRefineThreads) keys[m] = m < M ? order_key(g[m], m) : 0ull;
     __syncthreads();
     bitonic_desc(keys, P, kRefineThreads);
@@ -451,7 +475,11 @@ cast_status_t launch_coupled(const void* q, const void* k, const void* v, const 
   int P = 2;
   while (P < M) P <<= 1;
   const size_t shm2 = (size_t)P * 8 + (size_t)M * 4 + (size_t)((n_a * M + 31) / 32) * 4;
-  hipLaunchKernelGGL(coupled_refine_kernel, dim3(H), dim3(kRefineThreads), shm2, stream, a);
+  if (n_a * M <= kRefineCacheU)
+    hipLaunchKernelGGL(coupled_refine_kernel<true>, dim3(H), dim3(kRefineThreads),
+                       shm2 + (size_t)n_a * M * 4, stream, a);
+  else
+    hipLaunchKernelGGL(coupled_refine_kernel<false>, dim3(H), dim3(kRefineThreads), shm2, stream, a);
   return check_launch("coupled_refine");
 }
 

@@ -168,3 +168,13 @@ def test_coupled_long_history(cast_lib):
     anchors, n_frames = (0, 4, 8, 12), 16
     (exact, loose), _ = run_case(cast_lib, w, anchors, n_frames, 32)
     assert exact >= w.H // 3      # 32 of 128 dense values: near-ties are common
+
+
+def test_coupled_large_mask(cast_lib):
+    """n_a * M above what the solver stages in LDS (8192 values of u per head): u is
+    then read from global memory; three anchors, 3000 chunks of 2 tokens."""
+    w = gen.get(W.TINY)
+    anchors, n_frames = (0, 2, 4), 6
+    ww = W.Workload(**{**w.__dict__, "anchors": anchors})
+    (exact, loose), idx = run_case(cast_lib, ww, anchors, n_frames, 16, M=3000, Bv=2)
+    assert exact + loose == w.H
