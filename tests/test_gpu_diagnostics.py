@@ -34,10 +34,11 @@ MAX_ILL = 0.02           # at most this fraction of the columns may be ill-condi
 def corrections_check(ref64, got_p, got_m, want_p, want_m, t, a, b, alpha, tile):
     """rel-RMS of the corrections of frame t over its well-conditioned tile
     columns, after checking the spectral moduli of the others."""
+    th, tw = (tile, tile) if np.isscalar(tile) else tile
     Hg, Wg, D = ref64.shape[1:]
     well = np.ones((Hg, Wg, D), dtype=bool)
     n_ill = 0
-    for (y0, hp, x0, wp) in OP.tiles(Hg, Wg, tile, tile):
+    for (y0, hp, x0, wp) in OP.tiles(Hg, Wg, th, tw):
         sl = (slice(y0, y0 + hp), slice(x0, x0 + wp))
         Ft = OP.rfft2_ortho(ref64[t][sl])
         Fl = (1.0 - alpha) * OP.rfft2_ortho(ref64[a][sl]) + alpha * OP.rfft2_ortho(ref64[b][sl])
@@ -54,7 +55,7 @@ def corrections_check(ref64, got_p, got_m, want_p, want_m, t, a, b, alpha, tile)
             norm = np.sqrt((np.abs(F[:, :, ill]) ** 2).sum(axis=(0, 1)))
             err = np.abs(np.abs(G) - np.abs(F[:, :, ill])).max(axis=(0, 1))
             assert (err <= MOD_ABS * norm).all(), (t, y0, x0, err.max())
-    n_cols = len(OP.tiles(Hg, Wg, tile, tile)) * D
+    n_cols = len(OP.tiles(Hg, Wg, th, tw)) * D
     assert n_ill <= MAX_ILL * n_cols, (t, n_ill, n_cols)
     r = max(rel_rms(got_p[well], want_p[well]), rel_rms(got_m[well], want_m[well]))
     return r, n_ill
@@ -62,20 +63,21 @@ def corrections_check(ref64, got_p, got_m, want_p, want_m, t, a, b, alpha, tile)
 
 def run_case(cast_lib, ref_np, anchors, label, tile=8, edges=(0.0, 1 / 3, 2 / 3, 1.0), corr=True):
     dev = "cuda"
+    th, tw = (tile, tile) if np.isscalar(tile) else tile
     edges = [float(np.float32(e)) for e in edges]      # the values the kernel sees
     ref = torch.from_numpy(ref_np.astype(np.float32)).to(dev)
-    prm = cast_lib.cast_par_params_default(tile_h=tile, tile_w=tile)
+    prm = cast_lib.cast_par_params_default(tile_h=th, tile_w=tw)
     s1, _ = cast_lib.par_debug_shapes(len(anchors), ref.shape[1], ref.shape[2], prm)
     theta = torch.zeros(s1, device=dev)
     approx = torch.zeros_like(ref)
     cast_lib.cast_par_reconstruct(ref, anchors, prm, out=approx, theta_out=theta)
-    dprm = cast_lib.cast_diag_params_default(band_edges=edges, tile_h=tile, tile_w=tile)
+    dprm = cast_lib.cast_diag_params_default(band_edges=edges, tile_h=th, tile_w=tw)
     got = cast_lib.cast_spectral_diagnostics(ref, approx, anchors, dprm, theta=theta,
                                              want_corrections=corr)
     torch.cuda.synchronize()
     ref64 = ref.cpu().numpy().astype(np.float64)
     app64 = approx.cpu().numpy().astype(np.float64)
-    want = DG.frame_diagnostics(ref64, app64, anchors, OP.ParParams(tile_h=tile, tile_w=tile), edges)
+    want = DG.frame_diagnostics(ref64, app64, anchors, OP.ParParams(tile_h=th, tile_w=tw), edges)
     nr = got["nrmse"].cpu().numpy()
     bd = got["bands"].cpu().numpy()
     pe = got["phase_err"].cpu().numpy()
@@ -166,3 +168,15 @@ def test_diag_one_and_eight_bands(cast_lib):
     got = run_case(cast_lib, ref, (0, 3), "one band", edges=(0.0, 1.0), corr=False)
     assert np.allclose(got["bands"][1:3].cpu().numpy(), 1.0, atol=1e-6)
     run_case(cast_lib, ref, (0, 3), "eight bands", edges=tuple(np.linspace(0.0, 1.0, 9)), corr=False)
+
+
+def test_diag_tile_shapes(cast_lib):
+    """Tile shapes with edges 1, 2, 3 and 7 (each shape has its own kernel):
+    15x9 with 8x8 tiles gives 8x8, 8x1, 7x8 and 7x1; 5x7 with 2x3 tiles gives
+    2x3, 2x1, 1x3 and 1x1."""
+    rng = np.random.default_rng(13)
+    for (Hg, Wg, D, tile) in [(15, 9, 40, 8), (5, 7, 300, (2, 3))]:
+        base = rng.standard_normal((Hg, Wg, D))
+        ref = np.stack([np.roll(base, (t, -t), axis=(0, 1)) + 0.3 * rng.standard_normal((Hg, Wg, D))
+                        for t in range(5)])
+        run_case(cast_lib, ref, (0, 2, 4), f"{Hg}x{Wg}x{D} tile {tile}", tile=tile)
