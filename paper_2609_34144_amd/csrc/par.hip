@@ -6,10 +6,11 @@
 //              writes its per-bin products F_b conj(F_a) and |F_b||F_a|; the 64
 //              lanes are summed through LDS in fixed lane order into one partial
 //              per (pair, tile, channel block).                        (eq:cross)
-//   par_gate   grid (tile, pair): one lane per stored bin sums the partials in
-//              fixed order, then computes eta, reliability, theta (representative
-//              / mirror / self-conjugate), c_p, nu, g, and the per-target blend
-//              coefficients A_t = (1-alpha) e^{i g alpha theta} / (Hp Wp) and
+//   par_gate   grid (tile, pair, chunk of kGateTargets targets): one lane per
+//              stored bin sums the partials in fixed order, then computes eta,
+//              reliability, theta (representative / mirror / self-conjugate), c_p,
+//              nu, g, and the blend coefficients of the chunk's targets
+//              A_t = (1-alpha) e^{i g alpha theta} / (Hp Wp) and
 //              B_t = alpha e^{-i g (1-alpha) theta} / (Hp Wp).
 //                                              (App. A.2, eq:confidence, eq:gate)
 //   par_recon  grid (tile, channel block, pair): every lane re-transforms the two
@@ -35,7 +36,7 @@ template <int HP, int WP>
 __global__ __launch_bounds__(64) void par_xspec_kernel(ParArgs a, TileClass k,
                                                         const float* __restrict__ resid,
                                                         float* __restrict__ partial) {
-  __shared__ float lds[kChb * kLdsStride];
+  __shared__ float lds[kChb * kXsStride];
   xspec_block<HP, WP>(a, class_tile(a, k, blockIdx.x), blockIdx.y, blockIdx.z, resid, partial, lds);
 }
 
@@ -57,6 +58,8 @@ __device__ __forceinline__ float wrap_arg(float y, float x) {
   const float kPiF = 3.14159265358979323846f;
   return (t == -kPiF) ? kPiF : t;
 }
+
+constexpr int kGateTargets = 8;   // targets per gate block
 
 __global__ __launch_bounds__(64) void par_gate_kernel(ParArgs a, const float* __restrict__ partial,
                                                        float4* __restrict__ coef) {
@@ -117,36 +120,37 @@ __global__ __launch_bounds__(64) void par_gate_kernel(ParArgs a, const float* __
     gate = 1.0f / (1.0f + expf(-(conf - tau) / a.T));
   }
   // optional diagnostics, laid out per the caller's tile_h x (tile_w/2+1) rows
+  // (written by the first target chunk)
   const int nkx_out = a.tile_w / 2 + 1;
-  if (b < kBins && ky < a.tile_h && kx < nkx_out) {
+  if (blockIdx.z == 0 && b < kBins && ky < a.tile_h && kx < nkx_out) {
     const long long o = ((long long)pair * a.n_tiles + tile) * a.bins_out + ky * nkx_out + kx;
     if (a.theta_out) a.theta_out[o] = active ? theta : 0.0f;
     if (a.gate_out) a.gate_out[o] = active ? gate : 0.0f;
   }
-  if (a.conf_out && b == 0) a.conf_out[(long long)pair * a.n_tiles + tile] = conf;
+  if (a.conf_out && b == 0 && blockIdx.z == 0) a.conf_out[(long long)pair * a.n_tiles + tile] = conf;
   if (b >= kBins) return;
-  // blend coefficients for every target of this pair (eq:block composition)
+  // blend coefficients of this chunk of the pair's targets (eq:block composition):
+  // target k of the pair is fa+1+k for the interior, then (first pair) the frames
+  // before the first anchor, then (last pair) the frames after the last anchor
   const int n_pairs = a.n_anchor - 1;
   const int fa = a.anchors[pair], fb = a.anchors[pair + 1];
+  const int n_in = fb - fa - 1, n_lo = pair == 0 ? fa : 0;
+  const int n_hi = pair == n_pairs - 1 ? a.n_frames - fb - 1 : 0;
+  const int k0 = blockIdx.z * kGateTargets, k1 = min(k0 + kGateTargets, n_in + n_lo + n_hi);
   const float inv_gap = 1.0f / (float)(fb - fa);
   const float nrm = 1.0f / (float)(H * W);
-  for (int part = 0; part < 3; ++part) {
-    int t0, t1;
-    if (part == 0) { t0 = fa + 1; t1 = fb; }
-    else if (part == 1) { if (pair != 0) continue; t0 = 0; t1 = fa; }
-    else { if (pair != n_pairs - 1) continue; t0 = fb + 1; t1 = a.n_frames; }
-    for (int t = t0; t < t1; ++t) {
-      const float alpha = (float)(t - fa) * inv_gap;
-      float4 cf = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-      if (active) {
-        float sa, ca, sb, cb;
-        sincosf(gate * alpha * theta, &sa, &ca);
-        sincosf(-gate * (1.0f - alpha) * theta, &sb, &cb);
-        const float wa = (1.0f - alpha) * nrm, wb = alpha * nrm;
-        cf = make_float4(wa * ca, wa * sa, wb * cb, wb * sb);
-      }
-      coef[((long long)t * a.n_tiles + tile) * kBins + b] = cf;
+  for (int k = k0; k < k1; ++k) {
+    const int t = k < n_in ? fa + 1 + k : (k < n_in + n_lo ? k - n_in : fb + 1 + (k - n_in - n_lo));
+    const float alpha = (float)(t - fa) * inv_gap;
+    float4 cf = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if (active) {
+      float sa, ca, sb, cb;
+      sincosf(gate * alpha * theta, &sa, &ca);
+      sincosf(-gate * (1.0f - alpha) * theta, &sb, &cb);
+      const float wa = (1.0f - alpha) * nrm, wb = alpha * nrm;
+      cf = make_float4(wa * ca, wa * sa, wb * cb, wb * sb);
     }
+    coef[((long long)t * a.n_tiles + tile) * kBins + b] = cf;
   }
 }
 
@@ -298,6 +302,16 @@ cast_status_t launch_par(const float* resid, const int* anchors, int n_anchor, i
   a.accumulate = p.accumulate;
   a.update_anchors = p.update_anchors;
   for (int j = 0; j < n_anchor; ++j) a.anchors[j] = (short)anchors[j];
+  // gate grid: (tile, pair, chunk of kGateTargets targets of the pair)
+  int max_targets = 0;
+  for (int pr = 0; pr + 1 < n_anchor; ++pr) {
+    int n = anchors[pr + 1] - anchors[pr] - 1;
+    if (pr == 0) n += anchors[0];
+    if (pr + 2 == n_anchor) n += n_frames - anchors[n_anchor - 1] - 1;
+    max_targets = n > max_targets ? n : max_targets;
+  }
+  const dim3 gate_grid(pl.n_tiles, pl.n_pairs,
+                       max_targets > 0 ? (max_targets + kGateTargets - 1) / kGateTargets : 1);
 
   cast_status_t st;
   if (p.tile_h == 8 && p.tile_w == 8) {
@@ -318,7 +332,7 @@ cast_status_t launch_par(const float* resid, const int* anchors, int n_anchor, i
     hipLaunchKernelGGL(row.xspec[wi], grid, dim3(kChb), 0, stream, a, cs, resid, partial);
     st = check_launch("par_xspec");
     if (st != CAST_OK) return st;
-    hipLaunchKernelGGL(par_gate_kernel, dim3(pl.n_tiles, pl.n_pairs), dim3(64), 0, stream, a,
+    hipLaunchKernelGGL(par_gate_kernel, gate_grid, dim3(64), 0, stream, a,
                        (const float*)partial, coef);
     st = check_launch("par_gate");
     if (st != CAST_OK) return st;
@@ -336,7 +350,7 @@ cast_status_t launch_par(const float* resid, const int* anchors, int n_anchor, i
     st = check_launch("par_xspec");
     if (st != CAST_OK) return st;
   }
-  hipLaunchKernelGGL(par_gate_kernel, dim3(pl.n_tiles, pl.n_pairs), dim3(64), 0, stream, a,
+  hipLaunchKernelGGL(par_gate_kernel, gate_grid, dim3(64), 0, stream, a,
                      (const float*)partial, coef);
   st = check_launch("par_gate");
   if (st != CAST_OK) return st;

@@ -12,7 +12,7 @@ namespace pardev {
 constexpr int kBins = kParBinsMax;     // 40 stored-bin slots: index ky*5 + kx
 constexpr int kNkx = kParNkxMax;       // 5
 constexpr int kVals = kBins * 3;       // (Re Z, Im Z, W) per slot
-constexpr int kLdsStride = kVals + 1;  // odd row stride: conflict-free LDS transpose
+constexpr int kXsStride = kBins + 1;   // odd row stride: conflict-free LDS transpose
 constexpr int kChb = 64;               // channels per block (one wave)
 
 struct ParArgs {
@@ -83,14 +83,12 @@ __host__ __device__ constexpr bool self_conj(int ky, int kx, int H, int W) {
 
 // Unnormalised forward 2-D real DFT of one channel of one tile, kept on the
 // unique bins only: Hermitian columns ky <= HP/2, other columns all ky.
-// `r` covers the frame, `tile0` is the byte offset of channel 0 of the tile's
-// top-left token, `c4` the lane's channel byte offset (always in range).
+// load_tile reads the tile's HP x WP values of one channel: `r` covers the frame,
+// `tile0` is the byte offset of channel 0 of the tile's top-left token, `c4` the
+// lane's channel byte offset (always in range); fwd_tile transforms them.
 template <int HP, int WP>
-__device__ __forceinline__ void load_fwd(__amdgpu_buffer_rsrc_t r, unsigned tile0, unsigned WgD4,
-                                         unsigned D4, unsigned c4, float (&fr)[HP][WP / 2 + 1],
-                                         float (&fi)[HP][WP / 2 + 1]) {
-  constexpr int NKX = WP / 2 + 1;
-  float x[HP][WP];
+__device__ __forceinline__ void load_tile(__amdgpu_buffer_rsrc_t r, unsigned tile0, unsigned WgD4,
+                                          unsigned D4, unsigned c4, float (&x)[HP][WP]) {
   fft::static_for<0, HP>([&](auto yy) {
     constexpr int y = decltype(yy)::value;
     fft::static_for<0, WP>([&](auto xx) {
@@ -98,6 +96,13 @@ __device__ __forceinline__ void load_fwd(__amdgpu_buffer_rsrc_t r, unsigned tile
       x[y][xi] = buf_ld(r, c4, tile0 + y * WgD4 + xi * D4);
     });
   });
+}
+
+// Forward transform of loaded tile values (unique bins, as above).
+template <int HP, int WP>
+__device__ __forceinline__ void fwd_tile(const float (&x)[HP][WP], float (&fr)[HP][WP / 2 + 1],
+                                         float (&fi)[HP][WP / 2 + 1]) {
+  constexpr int NKX = WP / 2 + 1;
   float rr[HP][NKX], ri[HP][NKX];
   fft::static_for<0, HP>([&](auto yy) {
     constexpr int y = decltype(yy)::value;
@@ -134,61 +139,67 @@ __device__ __forceinline__ void load_fwd(__amdgpu_buffer_rsrc_t r, unsigned tile
 // ---------------------------------------------------------------------------
 // par_xspec
 // ---------------------------------------------------------------------------
+// One block of the cross-spectrum pass: tile `tile`, channel block `chb`, pair.
+// Every lane transforms both anchors of its channel (all their loads in flight
+// together); the per-bin products Re(F_b conj F_a), Im(F_b conj F_a) and
+// |F_b||F_a| are summed over the 64 lanes through LDS, one quantity at a time (a
+// 64 x 41 transpose, 10.5 KB, so that LDS does not limit the number of resident
+// blocks), in fixed lane order.
 template <int HP, int WP>
-__device__ __forceinline__ void xspec_body(const ParArgs& a, const float* __restrict__ resid,
-                                           const TileGeom& g, int c_lane, int fa, int fb,
-                                           float* lds_row) {
+__device__ __forceinline__ void xspec_block(const ParArgs& a, int tile, int chb, int pair,
+                                            const float* __restrict__ resid,
+                                            float* __restrict__ partial, float* lds) {
   constexpr int NKX = WP / 2 + 1;
+  const TileGeom g = tile_geom(a, tile);
+  const int lane = threadIdx.x;
+  const int c_lane = chb * kChb + lane;
+  const int fa = a.anchors[pair], fb = a.anchors[pair + 1];
   const bool valid = c_lane < a.D;
   const unsigned c4 = 4u * (unsigned)(valid ? c_lane : a.D - 1);
   const unsigned tile0 = 4u * (unsigned)((g.y0 * a.Wg + g.x0) * a.D);
   const unsigned WgD4 = 4u * (unsigned)(a.Wg * a.D), D4 = 4u * (unsigned)a.D;
   float ar[HP][NKX], ai[HP][NKX], br[HP][NKX], bi[HP][NKX];
-  load_fwd<HP, WP>(frame_rsrc(resid, fa, a.frame_elems), tile0, WgD4, D4, c4, ar, ai);
-  load_fwd<HP, WP>(frame_rsrc(resid, fb, a.frame_elems), tile0, WgD4, D4, c4, br, bi);
-  const float live = valid ? 1.0f : 0.0f;   // lanes past D contribute nothing
-  // every slot of the lane's LDS row is written (zeros where no unique bin lives)
-  fft::static_for<0, kNkx * HP>([&](auto bb) {
-    constexpr int ky = decltype(bb)::value / kNkx;
-    constexpr int kx = decltype(bb)::value % kNkx;
-    constexpr int s = (ky * kNkx + kx) * 3;
-    if constexpr (kx < NKX && ky < col_rows(kx, HP, WP)) {
-      const float xr = ar[ky][kx], xi = ai[ky][kx], yr = br[ky][kx], yi = bi[ky][kx];
-      lds_row[s + 0] = live * (yr * xr + yi * xi);
-      lds_row[s + 1] = self_conj(ky, kx, HP, WP) ? 0.0f : live * (yi * xr - yr * xi);
-      lds_row[s + 2] = live * sqrtf((xr * xr + xi * xi) * (yr * yr + yi * yi));
-    } else {
-      lds_row[s + 0] = 0.0f;
-      lds_row[s + 1] = 0.0f;
-      lds_row[s + 2] = 0.0f;
-    }
-  });
-  for (int s = HP * kNkx * 3; s < kVals; ++s) lds_row[s] = 0.0f;
-}
-
-// One block of the cross-spectrum pass: tile `tile`, channel block `chb`, pair.
-template <int HP, int WP>
-__device__ __forceinline__ void xspec_block(const ParArgs& a, int tile, int chb, int pair,
-                                            const float* __restrict__ resid,
-                                            float* __restrict__ partial, float* lds) {
-  const TileGeom g = tile_geom(a, tile);
-  const int lane = threadIdx.x;
-  const int c = chb * kChb + lane;
-  const int fa = a.anchors[pair], fb = a.anchors[pair + 1];
-  xspec_body<HP, WP>(a, resid, g, c, fa, fb, lds + lane * kLdsStride);
-  __syncthreads();
-  float* dst = partial + (((long long)pair * a.n_tiles + tile) * a.n_chblk + chb) * kVals;
-  for (int v = lane; v < kVals; v += kChb) {
-    float s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
-#pragma unroll 16
-    for (int l = 0; l < kChb; l += 4) {
-      s0 += lds[(l + 0) * kLdsStride + v];
-      s1 += lds[(l + 1) * kLdsStride + v];
-      s2 += lds[(l + 2) * kLdsStride + v];
-      s3 += lds[(l + 3) * kLdsStride + v];
-    }
-    dst[v] = (s0 + s1) + (s2 + s3);
+  {
+    float xa[HP][WP], xb[HP][WP];
+    load_tile<HP, WP>(frame_rsrc(resid, fa, a.frame_elems), tile0, WgD4, D4, c4, xa);
+    load_tile<HP, WP>(frame_rsrc(resid, fb, a.frame_elems), tile0, WgD4, D4, c4, xb);
+    fwd_tile<HP, WP>(xa, ar, ai);
+    fwd_tile<HP, WP>(xb, br, bi);
   }
+  const float live = valid ? 1.0f : 0.0f;   // lanes past D contribute nothing
+  float* row = lds + lane * kXsStride;
+  float* dst = partial + (((long long)pair * a.n_tiles + tile) * a.n_chblk + chb) * kVals;
+  fft::static_for<0, 3>([&](auto qq) {
+    constexpr int q = decltype(qq)::value;
+    // the lane's value of quantity q at every slot (zero where no unique bin lives)
+    fft::static_for<0, kNkx * HP>([&](auto bb) {
+      constexpr int ky = decltype(bb)::value / kNkx;
+      constexpr int kx = decltype(bb)::value % kNkx;
+      constexpr int s = ky * kNkx + kx;
+      if constexpr (kx < NKX && ky < col_rows(kx, HP, WP)) {
+        const float xr = ar[ky][kx], xi = ai[ky][kx], yr = br[ky][kx], yi = bi[ky][kx];
+        if constexpr (q == 0) row[s] = live * (yr * xr + yi * xi);
+        else if constexpr (q == 1) row[s] = self_conj(ky, kx, HP, WP) ? 0.0f : live * (yi * xr - yr * xi);
+        else row[s] = live * sqrtf((xr * xr + xi * xi) * (yr * yr + yi * yi));
+      } else {
+        row[s] = 0.0f;
+      }
+    });
+    for (int s = HP * kNkx; s < kBins; ++s) row[s] = 0.0f;
+    __syncthreads();
+    if (lane < kBins) {
+      float s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
+#pragma unroll 16
+      for (int l = 0; l < kChb; l += 4) {
+        s0 += lds[(l + 0) * kXsStride + lane];
+        s1 += lds[(l + 1) * kXsStride + lane];
+        s2 += lds[(l + 2) * kXsStride + lane];
+        s3 += lds[(l + 3) * kXsStride + lane];
+      }
+      dst[lane * 3 + q] = (s0 + s1) + (s2 + s3);
+    }
+    __syncthreads();
+  });
 }
 
 // ---------------------------------------------------------------------------
@@ -254,10 +265,14 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
   }
   float ar[HP][NKX], ai[HP][NKX];
   {
-    // F_b is parked in this lane's LDS column (LDS as extra per-lane storage: no
-    // other lane reads it, so no barrier is needed)
+    // both anchors' loads in flight together; F_b is parked in this lane's LDS
+    // column (LDS as extra per-lane storage: no other lane reads it, so no barrier
+    // is needed)
+    float xa[HP][WP], xb[HP][WP];
+    load_tile<HP, WP>(frame_rsrc(resid, fb, a.frame_elems), tile0, WgD4, D4, c4, xb);
+    load_tile<HP, WP>(frame_rsrc(resid, fa, a.frame_elems), tile0, WgD4, D4, c4, xa);
     float br[HP][NKX], bi[HP][NKX];
-    load_fwd<HP, WP>(frame_rsrc(resid, fb, a.frame_elems), tile0, WgD4, D4, c4, br, bi);
+    fwd_tile<HP, WP>(xb, br, bi);
     fft::static_for<0, NKX>([&](auto kk) {
       constexpr int kx = decltype(kk)::value;
       fft::static_for<0, col_rows(kx, HP, WP)>([&](auto yy) {
@@ -267,8 +282,8 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
         fb_lds[(2 * u + 1) * kChb] = bi[ky][kx];
       });
     });
+    fwd_tile<HP, WP>(xa, ar, ai);
   }
-  load_fwd<HP, WP>(frame_rsrc(resid, fa, a.frame_elems), tile0, WgD4, D4, c4, ar, ai);
   (void)NU;
   const int n_pairs = a.n_anchor - 1;
   for (int part = 0; part < 3; ++part) {
@@ -405,7 +420,7 @@ template <int HR, int WR>
 __global__ __launch_bounds__(64) void par_xspec_fused(ParArgs a, ClassSet cs,
                                                        const float* __restrict__ resid,
                                                        float* __restrict__ partial) {
-  __shared__ float lds[kChb * kLdsStride];
+  __shared__ float lds[kChb * kXsStride];
   for_class<HR, WR>(a, cs, blockIdx.x, [&](auto hp, auto wp, int tile) {
     xspec_block<decltype(hp)::value, decltype(wp)::value>(a, tile, blockIdx.y, blockIdx.z, resid,
                                                           partial, lds);
