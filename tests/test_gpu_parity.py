@@ -204,6 +204,26 @@ def test_attn_fast_and_aligned_modes(cast_lib, dh):
                    label=f"modes dh{dh} Bv{Bv}")
 
 
+@pytest.mark.parametrize("Bv,k_eff,n0", [(64, 96, 0), (72, 70, 0), (40, 80, 13)])
+def test_attn_many_routed_chunks(cast_lib, Bv, k_eff, n0):
+    """More than 64 routed chunks (the kernel keeps the first 64 chunk indices in a
+    register and reads the others from LDS), in the aligned (chunks of 64 rows),
+    fast (chunks of >= 64 rows) and general (current segment, short chunks) copy
+    modes; routed indices in arbitrary order with repeats."""
+    torch.manual_seed(300 + Bv)
+    dev = "cuda"
+    n_a, S, H, dh, M = 1, 70, 2, 128, 120
+    q = torch.randn(n_a, S, H, dh, device=dev).to(torch.bfloat16)
+    k = torch.randn(M, Bv, H, dh, device=dev).to(torch.bfloat16)
+    v = torch.randn(M, Bv, H, dh, device=dev).to(torch.bfloat16)
+    kc = torch.randn(max(n0, 1), H, dh, device=dev).to(torch.bfloat16) if n0 else None
+    vc = torch.randn(max(n0, 1), H, dh, device=dev).to(torch.bfloat16) if n0 else None
+    rng = np.random.default_rng(Bv)
+    idx = torch.tensor(rng.integers(0, M, size=(n_a, H, k_eff)), dtype=torch.int32, device=dev)
+    check_attn(cast_lib, q, k, v, idx, k_eff, 1 / math.sqrt(dh), kc=kc, vc=vc,
+               label=f"many chunks Bv{Bv} k{k_eff} n0 {n0}")
+
+
 def test_attn_topk_all_equals_dense(cast_lib):
     """topk = M routes every chunk: the result is dense attention over the whole history."""
     w = gen.get(W.TINY)
