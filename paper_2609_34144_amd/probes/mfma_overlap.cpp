@@ -1,8 +1,8 @@
 // Matrix-core ceiling of one MI355X and the cost of VALU work between a wave's own
 // MFMAs: the context for the attention kernel's roofline.
 //
-// One workgroup of 4 waves per CU (one wave per SIMD, as the attention kernel
-// runs), each wave a loop of 8 independent v_mfma_f32_32x32x16_bf16 chains with K
+// One workgroup of 4 waves per CU (one wave per SIMD, as the earlier single-wave
+// attention kernel ran), each wave a loop of 8 independent v_mfma_f32_32x32x16_bf16 chains with K
 // independent VALU instructions after every MFMA (K fused multiply-adds, or K
 // exponentials each followed by a multiply).  Prints the time per MFMA per wave;
 // with no VALU work that is the chip's sustained matrix-core rate:
