@@ -164,6 +164,10 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 2;                 // 0: group A, 1: group B
   const int l32 = lane & 31, hf = lane >> 5;
+  // a wave whose 32 queries all lie past S (in the last Q tile) skips its MFMA and
+  // softmax work but still takes part in the copies and barriers; the padded
+  // MFMAs would only draw power from the waves doing real work
+  const bool live = qt * kBQ + wave * 32 < a.S;
   // routed chunk indices of this (anchor, head), clamped into [0, M)
   // (entry k_eff repeats the last one, so a tile's "next slot" always names a real chunk)
   if (a.k_eff > 0) {
@@ -445,11 +449,11 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
     constexpr int P = decltype(par)::value;
     uint16_t* const kc = P == 0 ? lds_k0 : lds_k1;   // K[j]; then K[j+2]
     uint16_t* const vp = P == 0 ? lds_v1 : lds_v0;   // V[j-1]; then V[j+1]
-    mfma_phase(kc, vp);
+    if (live) mfma_phase(kc, vp);
     if (grp == 1) __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (grp == 1) issue_copies(j + 1, kc, vp);
-    if (j < nt) softmax_phase(j);
+    if (j < nt && live) softmax_phase(j);
     __syncthreads();
   };
   int j = 0;
