@@ -210,10 +210,13 @@ def main():
     del resid
     prm = cast.cast_par_params_default(accumulate=1)
     k_eff = min(w.topk, w.M) if w.has_attention else 0
-    route_ws = par_ws = None
+    route_ws = par_ws = attn_ws = None
     if w.has_attention and w.M > 0:
         nb = cast.cast_route_kv_workspace_bytes(w.n_a, w.S, w.H, w.dh, w.M, w.Bv)
         route_ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+        nb = cast.cast_anchor_attn_workspace_bytes(w.n_a, w.S, w.H, w.dh, k_eff, 0, w.Bv)
+        if nb > 0:
+            attn_ws = torch.empty(nb, dtype=torch.uint8, device=dev)
     if w.has_par:
         nb = cast.cast_par_workspace_bytes(w.n_frames, w.n_a, w.Hg, w.Wg, w.D, prm)
         par_ws = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
@@ -235,7 +238,7 @@ def main():
             if marks is not None:
                 marks[1].record(st)
             cast.cast_anchor_attn(s["q"], s["k"], s["v"], idx, ke, w.scale, out=attn_out,
-                                  stream=st)
+                                  workspace=attn_ws, stream=st)
         elif marks is not None:
             marks[1].record(st)
         if marks is not None:
@@ -411,7 +414,10 @@ def main():
     if w.has_attention:
         fl = attn_flops(w, k_eff)
         tf = fl / (attn_ms / 1e3) / 1e12
-        res["roofline"] = {"bound": "mfma", "kernel": f"anchor_attn_kernel<{w.dh}>",
+        # the attention call: anchor_attn_kernel, plus attn_merge_kernel when the
+        # units of a last partial round are split along the keys
+        kname = f"anchor_attn_kernel<{w.dh}>" + (" + attn_merge_kernel" if attn_ws is not None else "")
+        res["roofline"] = {"bound": "mfma", "kernel": kname,
                            "achieved": tf, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                            "frac": tf / PEAK_BF16_TFLOPS, "traffic": traffic.get("attn"),
                            "algorithmic_per_launch": fl}

@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define CAST_ABI_VERSION 1
+#define CAST_ABI_VERSION 2
 
 typedef enum {
   CAST_OK = 0,
@@ -201,13 +201,28 @@ cast_status_t cast_route_coupled(const void* q, const void* k_hist, const void* 
  * out      bf16 [n_a, S, H, dh] device (must not alias the inputs).
  * lse_out  fp32 [n_a, H, S] device natural-log sum of exp of the scaled logits,
  *          or NULL to skip.
+ * workspace  device scratch, or NULL.  The work is n_a * H * ceil(S / 256) units
+ *          (anchor, head, 256-query tile).  With a workspace, the units of a last,
+ *          at most half-full round on the device's compute units run as 2..8
+ *          pieces over disjoint key ranges and are merged (the softmax of each
+ *          piece renormalised by its log-sum-exp), which shortens that round;
+ *          results agree with the unsplit run to fp32 rounding before the bf16
+ *          output.  A non-NULL workspace must be 256-byte aligned and hold
+ *          cast_anchor_attn_workspace_bytes(...) bytes (CAST_ERR_WORKSPACE
+ *          otherwise); NULL runs every unit whole.  Owned by the caller; its
+ *          contents need no initialisation and are garbage after the call.
  */
 cast_status_t cast_anchor_attn(const void* q, const void* k_hist, const void* v_hist,
                                const int32_t* idx, int k_eff,
                                const void* k_cur, const void* v_cur, int n0,
                                int n_a, int S, int H, int dh, int M, int Bv,
                                float scale, void* out, float* lse_out,
-                               hipStream_t stream);
+                               void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes cast_anchor_attn uses for these sizes on the CURRENT device
+ * (0: nothing is split, or the sizes are invalid, or no device is visible). */
+size_t cast_anchor_attn_workspace_bytes(int n_a, int S, int H, int dh, int k_eff, int n0,
+                                        int Bv);
 
 /* ------------------------------------------------------------------------- */
 /* Phase-Aware Reconstruction (Sec. 4.3; App. A.2; eq:block)                 */

@@ -22,7 +22,8 @@ STATUS_NAMES = {0: "CAST_OK", 1: "CAST_ERR_NULL", 2: "CAST_ERR_SHAPE", 3: "CAST_
                 4: "CAST_ERR_UNSUPPORTED", 5: "CAST_ERR_WORKSPACE", 6: "CAST_ERR_HIP"}
 
 EXPORTED = ["cast_status_string", "cast_last_error_detail", "cast_abi_version",
-            "cast_route_kv_workspace_bytes", "cast_route_kv", "cast_anchor_attn",
+            "cast_route_kv_workspace_bytes", "cast_route_kv", "cast_anchor_attn_workspace_bytes",
+            "cast_anchor_attn",
             "cast_par_params_default", "cast_par_workspace_bytes", "cast_par_reconstruct",
             "cast_coupled_params_default", "cast_wo_gram", "cast_route_coupled_workspace_bytes",
             "cast_route_coupled", "cast_select_params_default",
@@ -90,7 +91,9 @@ def load(path: str = LIB_PATH):
                                   _c.POINTER(_i), _vp, _sz, _vp]
     lib.cast_anchor_attn.restype = _i
     lib.cast_anchor_attn.argtypes = [_vp, _vp, _vp, _vp, _i, _vp, _vp, _i, _i, _i, _i, _i, _i,
-                                     _i, _f, _vp, _vp, _vp]
+                                     _i, _f, _vp, _vp, _vp, _sz, _vp]
+    lib.cast_anchor_attn_workspace_bytes.restype = _sz
+    lib.cast_anchor_attn_workspace_bytes.argtypes = [_i] * 7
     lib.cast_par_params_default.restype = None
     lib.cast_par_params_default.argtypes = [_c.POINTER(ParParams)]
     lib.cast_par_workspace_bytes.restype = _sz
@@ -336,9 +339,16 @@ def cast_spectral_diagnostics(ref, approx, anchors, params: DiagParams | None = 
     return {"nrmse": nrmse, "bands": bands, "phase_err": perr, "r_phase": rp, "r_mag": rm}
 
 
+def cast_anchor_attn_workspace_bytes(n_a, S, H, dh, k_eff, n0, Bv) -> int:
+    return load().cast_anchor_attn_workspace_bytes(n_a, S, H, dh, k_eff, n0, Bv)
+
+
 def cast_anchor_attn(q, k_hist, v_hist, idx, k_eff: int, scale: float, k_cur=None, v_cur=None,
-                     out=None, lse_out=None, want_lse: bool = False, stream=None):
-    """Routed block-sparse attention of the anchor frames; returns (out bf16, lse or None)."""
+                     out=None, lse_out=None, want_lse: bool = False, workspace=None,
+                     split: bool = True, stream=None):
+    """Routed block-sparse attention of the anchor frames; returns (out bf16, lse or None).
+    split=True uses `workspace` (allocated here when None) to split the units of a
+    last partial round along the keys; split=False runs every unit whole."""
     import torch
     lib = load()
     n_a, S, H, dh = q.shape
@@ -348,9 +358,13 @@ def cast_anchor_attn(q, k_hist, v_hist, idx, k_eff: int, scale: float, k_cur=Non
         out = torch.empty_like(q)
     if lse_out is None and want_lse:
         lse_out = torch.empty((n_a, H, S), dtype=torch.float32, device=q.device)
+    ws, wsb = None, 0
+    if split:
+        ws, wsb = _ws(lib.cast_anchor_attn_workspace_bytes(n_a, S, H, dh, k_eff, n0, Bv), q.device,
+                      workspace)
     _check(lib.cast_anchor_attn(_ptr(q), _ptr(k_hist), _ptr(v_hist), _ptr(idx), k_eff,
                                 _ptr(k_cur), _ptr(v_cur), n0, n_a, S, H, dh, M, Bv, scale,
-                                _ptr(out), _ptr(lse_out), _stream(stream)))
+                                _ptr(out), _ptr(lse_out), _ptr(ws), wsb, _stream(stream)))
     return out, lse_out
 
 

@@ -41,6 +41,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -71,6 +72,13 @@ struct AttnArgs {
   uint16_t* out;
   float* lse;
   int n_a, S, H, M, Bv, n0, k_eff, L, n_qt, nblocks;
+  int nt_all;                    // 64-key tiles of the whole key sequence
+  // work units (anchor, head, Q tile): the first n_full run whole, the last
+  // n_split run as `split` pieces over disjoint key-tile ranges, each writing a
+  // normalised fp32 partial output and its log2-domain log-sum-exp, merged after
+  int n_full, n_split, split;
+  float* part_o;                 // [n_split * split][kBQ][dh]
+  float* part_lse;               // [n_split * split][kBQ]
   unsigned long long bv_magic;   // ceil(2^40 / Bv): row / Bv = (row * magic) >> 40
   float sl2;                     // scale * log2(e)
   long long hist_bytes;          // extent of the K/V history tensors
@@ -90,11 +98,25 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
-// Block b runs on XCD b % 8; give each XCD a contiguous range of logical blocks.
-__device__ __forceinline__ int xcd_remap(int b, int nb) {
-  const int per = nb / 8, rem = nb % 8;
-  const int xcd = b % 8, j = b / 8;
-  return (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + j;
+// Block b runs on XCD b % 8, the blocks of one XCD in order of b / 8.  Each XCD
+// takes a contiguous range of whole units (so the Q tiles of one (anchor, head),
+// which read the same keys, share its L2), then a contiguous range of the pieces,
+// which it runs last, in the partial round at the end.  Piece p is piece
+// p / n_split of split unit n_full + p % n_split.  piece = -1 for a whole unit.
+__device__ __forceinline__ void block_work(int b, int nblocks, int n_full, int n_split,
+                                           int& unit, int& piece) {
+  const int x = b & 7, j = b >> 3;
+  const int qf = n_full >> 3, rf = n_full & 7;
+  const int fx = qf + (x < rf ? 1 : 0);           // whole units on XCD x
+  if (j < fx) {
+    unit = x * qf + min(x, rf) + j;
+    piece = -1;
+    return;
+  }
+  const int qn = nblocks >> 3, rn = nblocks & 7;
+  const int p = (x * qn + min(x, rn)) - (x * qf + min(x, rf)) + (j - fx);
+  piece = p / n_split;
+  unit = n_full + (p - piece * n_split);
 }
 
 // v_max3_f32 (the compiler forms it only from some max chains)
@@ -157,8 +179,15 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) uint16_t lds_v1[kBK * DH];
   __shared__ int sidx[kMaxKeff + 1];
 
-  const int logical = xcd_remap(blockIdx.x, a.nblocks);
-  const int pair = logical / a.n_qt, qt = logical - pair * a.n_qt;
+  int unit, piece;
+  block_work(blockIdx.x, a.nblocks, a.n_full, a.n_split, unit, piece);
+  const int pair = unit / a.n_qt, qt = unit - pair * a.n_qt;
+  // key tiles [tb, tb + nt) of the sequence's nt_all
+  int tb = 0, nt = a.nt_all;
+  if (piece >= 0) {
+    tb = piece * a.nt_all / a.split;
+    nt = (piece + 1) * a.nt_all / a.split - tb;
+  }
   const int i = pair / a.H, h = pair - (pair / a.H) * a.H;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -204,7 +233,6 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
   };
 
   const unsigned row_bytes = (unsigned)(a.H * DH * 2), head_bytes = (unsigned)(h * DH * 2);
-  const int nt = (a.L + kBK - 1) / kBK;
 
   // ---- copy slots.  The four waves of group B copy every tile: wave 4 + w takes
   //      K (and V) slots k = w + 4r, r < KSL / 4.  Slot k fills LDS chunks
@@ -291,19 +319,19 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
   };
   Cursor cur_k{}, cur_v{};
   if constexpr (FAST) {
-    cur_k = cursor_at(min(1, nt - 1));
-    cur_v = cursor_at(0);
+    cur_k = cursor_at(tb + min(1, nt - 1));
+    cur_v = cursor_at(tb);
   }
-  // copies(c): K[c + 1] and V[c] (those that exist)
+  // copies(c): K[c + 1] and V[c] (those that exist; c counts from tile tb)
   auto issue_copies = [&](int c, uint16_t* kdst, uint16_t* vdst) __attribute__((always_inline)) {
     if constexpr (FAST) {
-      if (c + 1 < nt) copy_tile(IC<0>{}, c + 1, cur_map(cur_k), kdst);
-      if (c < nt) copy_tile(IC<1>{}, c, cur_map(cur_v), vdst);
+      if (c + 1 < nt) copy_tile(IC<0>{}, tb + c + 1, cur_map(cur_k), kdst);
+      if (c < nt) copy_tile(IC<1>{}, tb + c, cur_map(cur_v), vdst);
       if (c + 2 < nt) advance(cur_k);
       if (c + 1 < nt) advance(cur_v);
     } else {
-      if (c + 1 < nt) copy_tile(IC<0>{}, c + 1, TileMap{}, kdst);
-      if (c < nt) copy_tile(IC<1>{}, c, TileMap{}, vdst);
+      if (c + 1 < nt) copy_tile(IC<0>{}, tb + c + 1, TileMap{}, kdst);
+      if (c < nt) copy_tile(IC<1>{}, tb + c, TileMap{}, vdst);
     }
   };
 
@@ -374,8 +402,8 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
   //      half-wave), exponentials packed to the bf16 P^T operands and summed,
   //      running sum, O rescale when the running max moved
   auto softmax_phase = [&](int j) __attribute__((always_inline)) {
-    if (j == nt - 1 && a.L != nt * kBK) {
-      const int key0 = j * kBK;
+    if (tb + j == a.nt_all - 1 && a.L != a.nt_all * kBK) {
+      const int key0 = (tb + j) * kBK;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -428,8 +456,8 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
     for (int x = tid; x < kBK * DH / 8; x += kThreads) z[x] = u32x4{0u, 0u, 0u, 0u};
   }
   if (grp == 1) {
-    if constexpr (FAST) copy_tile(IC<0>{}, 0, cur_map(cursor_at(0)), lds_k0);
-    else copy_tile(IC<0>{}, 0, TileMap{}, lds_k0);
+    if constexpr (FAST) copy_tile(IC<0>{}, tb, cur_map(cursor_at(tb)), lds_k0);
+    else copy_tile(IC<0>{}, tb, TileMap{}, lds_k0);
   }
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
@@ -464,10 +492,25 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
   if (j <= nt) iter(IC<0>{}, j);
   if (grp == 0) __syncthreads();   // B's extra interval at the start
 
-  // ---- epilogue: normalise, write O (bf16) and the log-sum-exp
+  // ---- epilogue: normalise, write O (bf16) and the log-sum-exp; a piece writes
+  //      its normalised fp32 partial and log2-domain log-sum-exp instead
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = 1.0f / l_tot;
-  if (qi < a.S) {
+  if (piece >= 0) {
+    if (qi < a.S) {
+      const long long slot = (long long)(unit - a.n_full) * a.split + piece;
+      const int ql = wave * 32 + l32;
+      float* po = a.part_o + (slot * kBQ + ql) * DH + 4 * hf;
+#pragma unroll
+      for (int db = 0; db < ND; ++db)
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4)
+          *reinterpret_cast<f32x4*>(po + db * 32 + 8 * g4) =
+              f32x4{acc_o[db][4 * g4 + 0] * inv, acc_o[db][4 * g4 + 1] * inv,
+                    acc_o[db][4 * g4 + 2] * inv, acc_o[db][4 * g4 + 3] * inv};
+      if (hf == 0) a.part_lse[slot * kBQ + ql] = m_run + __log2f(l_tot);
+    }
+  } else if (qi < a.S) {
     uint16_t* op = a.out + (((long long)i * a.S + qi) * a.H + h) * DH + 4 * hf;
 #pragma unroll
     for (int db = 0; db < ND; ++db)
@@ -482,26 +525,103 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
   }
 }
 
+// Merge of the pieces of each split unit: with l_p the log2-domain log-sum-exp
+// and O_p the normalised output of piece p over its key range,
+//   O = sum_p 2^(l_p - l_max) O_p / sum_p 2^(l_p - l_max),
+//   log-sum-exp = ln 2 (l_max + log2 sum_p 2^(l_p - l_max)).
+// One thread per (split unit, query of its tile, 4 channels).
+template <int DH>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
+  constexpr int PER_Q = DH / 4, PER_UNIT = kBQ * PER_Q;
+  const long long t = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (long long)a.n_split * PER_UNIT) return;
+  const int u = (int)(t / PER_UNIT), rem = (int)(t - (long long)u * PER_UNIT);
+  const int ql = rem / PER_Q, d4 = rem - ql * PER_Q;
+  const int unit = a.n_full + u;
+  const int pair = unit / a.n_qt, qt = unit - pair * a.n_qt;
+  const int i = pair / a.H, h = pair - i * a.H;
+  const int qi = qt * kBQ + ql;
+  if (qi >= a.S) return;
+  const long long slot0 = (long long)u * a.split;
+  float lmax = -INFINITY;
+  for (int p = 0; p < a.split; ++p) lmax = fmaxf(lmax, a.part_lse[(slot0 + p) * kBQ + ql]);
+  float wsum = 0.0f;
+  f32x4 acc{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int p = 0; p < a.split; ++p) {
+    const float w = exp2f(a.part_lse[(slot0 + p) * kBQ + ql] - lmax);
+    const f32x4 o = *reinterpret_cast<const f32x4*>(a.part_o + ((slot0 + p) * kBQ + ql) * DH + 4 * d4);
+    wsum += w;
+    acc += w * o;
+  }
+  const float inv = 1.0f / wsum;
+  uint16_t* op = a.out + (((long long)i * a.S + qi) * a.H + h) * DH + 4 * d4;
+  *reinterpret_cast<u32x2*>(op) = u32x2{pack_bf16x2(acc.x * inv, acc.y * inv), pack_bf16x2(acc.z * inv, acc.w * inv)};
+  if (a.lse && d4 == 0)
+    a.lse[((long long)i * a.H + h) * a.S + qi] = (lmax + log2f(wsum)) * 0.69314718055994531f;
+}
+
 template <int DH>
 cast_status_t launch_dh(AttnArgs a, hipStream_t stream) {
-  a.n_qt = (a.S + kBQ - 1) / kBQ;
-  a.nblocks = a.n_a * a.H * a.n_qt;
+  a.nblocks = a.n_full + a.n_split * a.split;
   if (a.n0 == 0 && a.Bv % kBK == 0)
     hipLaunchKernelGGL((anchor_attn_kernel<DH, 2>), dim3(a.nblocks), dim3(kThreads), 0, stream, a);
   else if (a.n0 == 0 && a.Bv >= kBK)
     hipLaunchKernelGGL((anchor_attn_kernel<DH, 1>), dim3(a.nblocks), dim3(kThreads), 0, stream, a);
   else
     hipLaunchKernelGGL((anchor_attn_kernel<DH, 0>), dim3(a.nblocks), dim3(kThreads), 0, stream, a);
+  if (a.n_split > 0) {
+    const long long threads = (long long)a.n_split * kBQ * (DH / 4);
+    hipLaunchKernelGGL((attn_merge_kernel<DH>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
+                       stream, a);
+  }
   return check_launch("anchor_attn");
 }
 
 }  // namespace
 
+AttnSplitPlan attn_split_plan(int n_a, int S, int H, int dh, long long L, int cus) {
+  constexpr long long kMaxSplit = 8, kMinPieceTiles = 16;
+  const long long units = (long long)n_a * H * ((S + kBQ - 1) / kBQ);
+  AttnSplitPlan p{(int)units, 0, 1, 0};
+  if (cus <= 0) return p;
+  const long long rem = units % cus;
+  if (rem == 0) return p;
+  const long long nt_all = (L + kBK - 1) / kBK;
+  long long s = cus / rem;
+  s = s < kMaxSplit ? s : kMaxSplit;
+  s = s < nt_all / kMinPieceTiles ? s : nt_all / kMinPieceTiles;
+  if (s < 2) return p;
+  p.n_full = (int)(units - rem);
+  p.n_split = (int)rem;
+  p.split = (int)s;
+  p.bytes = align_up((size_t)rem * s * kBQ * dh * 4) + align_up((size_t)rem * s * kBQ * 4);
+  return p;
+}
+
+int device_cu_count() {
+  // a benign race: concurrent first calls store the same value
+  static int cache[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return 0;
+    }
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
 cast_status_t launch_anchor_attn(const void* q, const void* k_hist, const void* v_hist,
                                  const int32_t* idx, int k_eff, const void* k_cur,
                                  const void* v_cur, int n0, int n_a, int S, int H, int dh, int M,
                                  int Bv, float scale, void* out, float* lse_out,
-                                 hipStream_t stream) {
+                                 const AttnSplitPlan& plan, void* workspace, hipStream_t stream) {
   AttnArgs a{};
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k_hist);
@@ -525,6 +645,16 @@ cast_status_t launch_anchor_attn(const void* q, const void* k_hist, const void* 
   a.sl2 = scale * 1.4426950408889634f;
   a.hist_bytes = k_eff > 0 ? (long long)M * Bv * H * dh * 2 : 0;
   a.cur_bytes = n0 > 0 ? (long long)n0 * H * dh * 2 : 0;
+  a.n_qt = (S + kBQ - 1) / kBQ;
+  a.nt_all = (a.L + kBK - 1) / kBK;
+  a.n_full = plan.n_full;
+  a.n_split = plan.n_split;
+  a.split = plan.split;
+  if (plan.n_split > 0) {
+    a.part_o = static_cast<float*>(workspace);
+    a.part_lse = reinterpret_cast<float*>(static_cast<char*>(workspace) +
+                                          align_up((size_t)plan.n_split * plan.split * kBQ * dh * 4));
+  }
   switch (dh) {
     case 32: return launch_dh<32>(a, stream);
     case 64: return launch_dh<64>(a, stream);

@@ -178,11 +178,18 @@ cast_status_t cast_route_coupled(const void* q, const void* k_hist, const void* 
 
 // ---------------------------------------------------------------- attention
 
+size_t cast_anchor_attn_workspace_bytes(int n_a, int S, int H, int dh, int k_eff, int n0, int Bv) {
+  if (n_a < 1 || S < 1 || H < 1 || !dh_ok(dh) || k_eff < 0 || n0 < 0 || Bv < 1) return 0;
+  const long long L = (long long)n0 + (long long)k_eff * Bv;
+  if (L < 1) return 0;
+  return attn_split_plan(n_a, S, H, dh, L, device_cu_count()).bytes;
+}
+
 cast_status_t cast_anchor_attn(const void* q, const void* k_hist, const void* v_hist,
                                const int32_t* idx, int k_eff, const void* k_cur,
                                const void* v_cur, int n0, int n_a, int S, int H, int dh, int M,
                                int Bv, float scale, void* out, float* lse_out,
-                               hipStream_t stream) {
+                               void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (n_a < 1 || S < 1 || H < 1 || M < 0 || Bv < 1 || n0 < 0 || k_eff < 0)
     return fail(CAST_ERR_SHAPE, "attn: need n_a,S,H,Bv>=1 and M,n0,k_eff>=0");
   if (!dh_ok(dh)) return fail(CAST_ERR_UNSUPPORTED, "attn: dh must be 32, 64 or 128 (got %d)", dh);
@@ -207,8 +214,17 @@ cast_status_t cast_anchor_attn(const void* q, const void* k_hist, const void* v_
   const void* ptrs[] = {q, k_hist, v_hist, k_cur, v_cur, out};
   for (const void* p : ptrs)
     if (p != nullptr && !aligned(p, 16)) return fail(CAST_ERR_SHAPE, "attn: tensors must be 16-byte aligned");
+  // no workspace: every unit runs whole
+  AttnSplitPlan plan{(int)((long long)n_a * H * ((S + 255) / 256)), 0, 1, 0};
+  if (workspace != nullptr) {
+    if (!aligned(workspace, kWsAlign))
+      return fail(CAST_ERR_WORKSPACE, "attn: workspace must be %zu-byte aligned", kWsAlign);
+    plan = attn_split_plan(n_a, S, H, dh, L, device_cu_count());
+    if (workspace_bytes < plan.bytes)
+      return fail(CAST_ERR_WORKSPACE, "attn: workspace has %zu bytes, %zu needed", workspace_bytes, plan.bytes);
+  }
   return launch_anchor_attn(q, k_hist, v_hist, idx, k_eff, k_cur, v_cur, n0, n_a, S, H, dh, M,
-                            Bv, scale, out, lse_out, stream);
+                            Bv, scale, out, lse_out, plan, workspace, stream);
 }
 
 // ---------------------------------------------------------------------- PAR

@@ -76,11 +76,24 @@ cast_status_t launch_wo_gram(const void* w_o, int D, int H, int dh, float* gram,
 // Attention
 // ---------------------------------------------------------------------------
 constexpr int kAttnMaxKeff = 1024;   // routed chunks per (anchor, head)
+// Key split of the routed attention.  With U = n_a H ceil(S / 256) work units
+// (anchor, head, 256-query tile) on C compute units, the last U mod C units (all
+// of them when U < C) form a partial round; when it is at most half full they run
+// as `split` pieces over disjoint key ranges (at most 8, each at least 16 key
+// tiles), which the pieces' partial outputs need `bytes` of workspace for.
+struct AttnSplitPlan {
+  int n_full, n_split, split;
+  size_t bytes;
+};
+AttnSplitPlan attn_split_plan(int n_a, int S, int H, int dh, long long L, int cus);
+// compute units of the current device (cached per device), 0 if they cannot be read
+int device_cu_count();
+
 cast_status_t launch_anchor_attn(const void* q, const void* k_hist, const void* v_hist,
                                  const int32_t* idx, int k_eff, const void* k_cur,
                                  const void* v_cur, int n0, int n_a, int S, int H, int dh, int M,
                                  int Bv, float scale, void* out, float* lse_out,
-                                 hipStream_t stream);
+                                 const AttnSplitPlan& plan, void* workspace, hipStream_t stream);
 
 // ---------------------------------------------------------------------------
 // PAR

@@ -62,7 +62,7 @@ def test_exports_every_declared_symbol(lib):
 def test_status_strings(lib):
     for code, name in cast.STATUS_NAMES.items():
         assert lib.cast_status_string(code).decode() == name
-    assert lib.cast_abi_version() == 1
+    assert lib.cast_abi_version() == 2
 
 
 def test_par_params_default_matches_paper(lib):
@@ -109,9 +109,9 @@ def test_route_bypass_m0(lib):
 
 
 def _attn(lib, *, q=A, k=2 * A, v=3 * A, idx=4 * A, k_eff=2, kc=None, vc=None, n0=0, n_a=2, S=64, H=2,
-          dh=32, M=4, Bv=64, scale=0.5, out=5 * A):
+          dh=32, M=4, Bv=64, scale=0.5, out=5 * A, ws=None, wsb=0):
     return lib.cast_anchor_attn(q, k, v, idx, k_eff, kc, vc, n0, n_a, S, H, dh, M, Bv, scale,
-                                out, None, None)
+                                out, None, ws, wsb, None)
 
 
 def test_attn_validation(lib):
@@ -123,6 +123,9 @@ def test_attn_validation(lib):
     assert _attn(lib, q=None) == NULL
     assert _attn(lib, idx=None) == NULL
     assert _attn(lib, n0=4) == NULL                      # k_cur / v_cur missing
+    assert _attn(lib, ws=6 * A + 8, wsb=1 << 20) == WORKSPACE   # misaligned workspace
+    assert lib.cast_anchor_attn_workspace_bytes(2, 64, 2, 48, 2, 0, 64) == 0   # bad dh
+    assert lib.cast_anchor_attn_workspace_bytes(2, 64, 2, 32, 0, 0, 64) == 0   # no keys
     assert _attn(lib, out=5 * A + 8) == SHAPE                   # misaligned
 
 

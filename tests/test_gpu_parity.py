@@ -132,9 +132,10 @@ def test_route_deterministic(cast_lib):
 # attention
 # ---------------------------------------------------------------------------
 
-def check_attn(cast_lib, q, k, v, idx, k_eff, scale, kc=None, vc=None, rows=None, label=""):
+def check_attn(cast_lib, q, k, v, idx, k_eff, scale, kc=None, vc=None, rows=None, label="",
+               split=True):
     out, lse = cast_lib.cast_anchor_attn(q, k, v, idx, k_eff, scale, k_cur=kc, v_cur=vc,
-                                         want_lse=True)
+                                         want_lse=True, split=split)
     torch.cuda.synchronize()
     O, L = OA.anchor_attention(np64(q), np64(k), np64(v), idx.cpu().numpy() if idx is not None
                                else np.zeros((q.shape[0], q.shape[2], 0), np.int32), scale,
@@ -222,6 +223,36 @@ def test_attn_many_routed_chunks(cast_lib, Bv, k_eff, n0):
     idx = torch.tensor(rng.integers(0, M, size=(n_a, H, k_eff)), dtype=torch.int32, device=dev)
     check_attn(cast_lib, q, k, v, idx, k_eff, 1 / math.sqrt(dh), kc=kc, vc=vc,
                label=f"many chunks Bv{Bv} k{k_eff} n0 {n0}")
+
+
+@pytest.mark.parametrize("dh", [32, 64, 128])
+@pytest.mark.parametrize("n_a,S,H,M,Bv,k_eff,n0", [
+    (1, 300, 2, 30, 100, 24, 37),    # general copy mode, 2 pieces, ragged key and query tails
+    (2, 256, 3, 128, 64, 128, 0),    # aligned mode, 8 pieces
+    (1, 70, 2, 64, 72, 60, 0),       # fast mode, 4 pieces, ragged last key tile
+])
+def test_attn_key_split(cast_lib, dh, n_a, S, H, M, Bv, k_eff, n0):
+    """Work units of a last partial round split along the keys (pieces merged by
+    their log-sum-exps): the split run and the unsplit run (no workspace) both
+    meet the oracle's bar, and they agree with each other to bf16 rounding."""
+    need = cast_lib.cast_anchor_attn_workspace_bytes(n_a, S, H, dh, k_eff, n0, Bv)
+    assert need > 0, "these sizes must take the split path"
+    torch.manual_seed(400 + dh + Bv)
+    dev = "cuda"
+    q = torch.randn(n_a, S, H, dh, device=dev).to(torch.bfloat16)
+    k = torch.randn(M, Bv, H, dh, device=dev).to(torch.bfloat16)
+    v = torch.randn(M, Bv, H, dh, device=dev).to(torch.bfloat16)
+    kc = torch.randn(n0, H, dh, device=dev).to(torch.bfloat16) if n0 else None
+    vc = torch.randn(n0, H, dh, device=dev).to(torch.bfloat16) if n0 else None
+    rng = np.random.default_rng(dh + Bv)
+    idx = torch.tensor(rng.integers(0, M, size=(n_a, H, k_eff)), dtype=torch.int32, device=dev)
+    a = check_attn(cast_lib, q, k, v, idx, k_eff, 1 / math.sqrt(dh), kc=kc, vc=vc,
+                   label=f"split dh{dh} Bv{Bv}")
+    b = check_attn(cast_lib, q, k, v, idx, k_eff, 1 / math.sqrt(dh), kc=kc, vc=vc,
+                   label=f"unsplit dh{dh} Bv{Bv}", split=False)
+    d = (a.float() - b.float()).abs().max().item()
+    log(f"[attn split vs unsplit dh{dh} Bv{Bv}] max-abs {d:.3e} (workspace {need} B)")
+    assert d <= 2.0 ** -7 * max(1.0, b.float().abs().max().item())
 
 
 def test_attn_topk_all_equals_dense(cast_lib):
