@@ -48,7 +48,7 @@ def sources_hash(part: str) -> str:
 def part_of(kernel: str) -> str | None:
     if "route_" in kernel:
         return "route"
-    if "anchor_attn" in kernel:
+    if "anchor_attn" in kernel or "attn_merge" in kernel:
         return "attn"
     if "par_" in kernel:
         return "par"
