@@ -230,6 +230,7 @@ def test_attn_many_routed_chunks(cast_lib, Bv, k_eff, n0):
     (1, 300, 2, 30, 100, 24, 37),    # general copy mode, 2 pieces, ragged key and query tails
     (2, 256, 3, 128, 64, 128, 0),    # aligned mode, 8 pieces
     (1, 70, 2, 64, 72, 60, 0),       # fast mode, 4 pieces, ragged last key tile
+    (1, 320, 2, 40, 64, 40, 0),      # last Q tile of exactly two live waves, aligned mode
 ])
 def test_attn_key_split(cast_lib, dh, n_a, S, H, M, Bv, k_eff, n0):
     """Work units of a last partial round split along the keys (pieces merged by
