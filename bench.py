@@ -167,9 +167,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="matrix_game_like_8f30x52_d1536")
+    ap.add_argument("--workload", default="hy_world_like_16f44x80_d3072")
     ap.add_argument("--seed", type=int, default=42)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--step-only", action="store_true",
+                    help="time the block step and its calls only (no coupled routing, block "
+                         "update, frame selection or diagnostics), e.g. under a kernel trace")
     ap.add_argument("--graph", action="store_true",
                     help="replay the timed steps as captured HIP graphs instead of launching them")
     args = ap.parse_args()
@@ -282,22 +285,44 @@ def main():
     torch.cuda.synchronize()
     ms_total = t_start.elapsed_time(t_end)
     ms_step = ms_total / args.steps
-    # the per-call breakdown, in a second pass with events between the calls (the
-    # events themselves add gaps, so this pass does not give the step time)
-    marks = [[ev() for _ in range(4)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    for i in range(args.steps):
-        step(sets[i % N_COPIES], marks[i])
-    torch.cuda.synchronize()
-    per_call = {"route": [m[0].elapsed_time(m[1]) for m in marks],
-                "attn": [m[1].elapsed_time(m[2]) for m in marks],
-                "par": [m[2].elapsed_time(m[3]) for m in marks]}
-    route_ms, attn_ms, par_ms = (float(np.mean(per_call[c])) for c in ("route", "attn", "par"))
+    # the per-call breakdown: each call launched alone `steps` times back to back
+    # (cycling over the input copies) between one pair of events on its stream, so
+    # a call's average is its kernels' duration plus the launch gaps between them,
+    # as a kernel trace sees it; the route indices for attention come from a
+    # routing pass per copy before its loop
+    def timed_loop(fn):
+        a, b = ev(), ev()
+        torch.cuda.synchronize()
+        a.record(stream)
+        for i in range(args.steps):
+            fn(sets[i % N_COPIES])
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / args.steps
+
+    per_call = {}
+    route_ms = attn_ms = 0.0
+    if w.has_attention:
+        route_ms = timed_loop(lambda s: cast.cast_route_kv(s["q"], s["k"], w.topk, w.scale,
+                                                           idx_out=idx, workspace=route_ws,
+                                                           stream=stream))
+        idx_c = []
+        for c in range(N_COPIES):
+            ic = torch.empty_like(idx)
+            cast.cast_route_kv(sets[c]["q"], sets[c]["k"], w.topk, w.scale, idx_out=ic,
+                               workspace=route_ws, stream=stream)
+            sets[c]["idx"] = ic
+        attn_ms = timed_loop(lambda s: cast.cast_anchor_attn(s["q"], s["k"], s["v"], s["idx"],
+                                                             k_eff, w.scale, out=attn_out,
+                                                             workspace=attn_ws, stream=stream))
+    par_ms = timed_loop(lambda s: cast.cast_par_reconstruct(
+        s["resid"], w.anchors, prm, out=s["x"], workspace=par_ws, stream=stream)) if w.has_par else 0.0
+    per_call.update(route=route_ms, attn=attn_ms, par=par_ms)
 
     # reconstruction-coupled routing (NEXT-1), timed on its own after the step;
     # the W_O Gram matrices depend on weights only and are prepared once, untimed
     coupled_ms = None
-    if w.has_attention and w.M > 0:
+    if w.has_attention and w.M > 0 and not args.step_only:
         gram = cast.cast_wo_gram(gen.wo_weight(w.D, device=dev), w.H, w.dh)
         cprm = cast.cast_coupled_params_default()
         nb = cast.cast_route_coupled_workspace_bytes(w.n_a, w.S, w.H, w.dh, w.M, w.Bv)
@@ -323,7 +348,7 @@ def main():
     # the whole update of one residual site (e.g. the FFN site): PAR of the skipped
     # frames with every anchor's own update fused in, timed on its own
     block_ms = None
-    if w.has_par:
+    if w.has_par and not args.step_only:
         bprm = cast.cast_par_params_default(accumulate=1, update_anchors=1)
         bm = [[ev(), ev()] for _ in range(args.steps)]
         for i in range(args.warmup):
@@ -344,7 +369,7 @@ def main():
     # control-aware frame selection for the next block (both control branches, bf16),
     # timed on its own
     sel_ms = None
-    if w.n_frames >= 2:
+    if w.n_frames >= 2 and not args.step_only:
         ctl = [gen.control_inputs(w, seed=args.seed + c, device=dev) for c in range(N_COPIES)]
         ages = torch.zeros(w.n_frames, dtype=torch.int32, device=dev)
         sel_out = torch.empty(len(w.anchors), dtype=torch.int32, device=dev)
@@ -370,7 +395,7 @@ def main():
     # spectral diagnostics of the skipped frames (validation, not inference): error
     # ratio, band energies, transport phase error and both oracle corrections
     diag_ms = None
-    if w.has_par:
+    if w.has_par and not args.step_only:
         s1, _ = cast.par_debug_shapes(w.n_a, w.Hg, w.Wg, prm)
         theta = torch.zeros(s1, device=dev)
         s0 = sets[0]
@@ -407,7 +432,8 @@ def main():
         "per_call_ms": {"route": route_ms, "attn": attn_ms, "par": par_ms,
                         "route_coupled": coupled_ms, "par_block_update": block_ms,
                         "frame_select": sel_ms, "spectral_diagnostics": diag_ms},
-        "per_call_ms_median": {c: float(np.median(v)) for c, v in per_call.items()},
+        "per_call_ms_median": {c: float(np.median(v)) for c, v in per_call.items()
+                               if isinstance(v, list)},
     }
     extra = {}
     traffic = load_traffic(w.name)

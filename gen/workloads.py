@@ -303,3 +303,96 @@ def par_inputs(w: Workload, seed: int = 42, frames="anchors", D=None, Hg=None, W
     x0 = np.random.default_rng(s_x).standard_normal((n, Hg, Wg, D)).astype(np.float32) \
         if n * Hg * Wg * D <= (1 << 27) else None
     return resid, x0, info
+
+
+# ---------------------------------------------------------------------------
+# Designed-spectrum tiles (input construction for the reliability threshold of
+# App. A.2): a real tile whose orthonormal half-spectrum holds prescribed values
+# per channel, so that bins fall on either side of the threshold by design.
+# ---------------------------------------------------------------------------
+
+def _pol(r, phi):
+    return r * complex(math.cos(phi), math.sin(phi))
+
+
+# Entries (ky, kx, channel, F_a, F_b) of an 8x8 tile, D >= 2; every other stored
+# bin is zero.  Column kx = 0 is listed Hermitian-consistent ((2,0) and (6,0)).
+# With max W = 4 at DC the threshold is 4e-6 + 1e-8; bin (2,1) sits at about 3x it,
+# bin (3,1) at 0.75x, bin (1,3) at 0.3x, and bin (1,2) has W = 0.02 but its two
+# channels cancel in Z down to 1e-8.
+_S1, _S2, _S3 = math.sqrt(1.2e-5), math.sqrt(3e-6), math.sqrt(1.2e-6)
+RELIABILITY_TILE = (
+    (0, 0, 0, 2.0, 2.0),
+    (1, 1, 0, 1.0, _pol(1.0, math.pi / 3)),
+    (1, 1, 1, 1.0, 1.0),
+    (2, 1, 0, _S1, _pol(_S1, -math.pi / 4)),
+    (3, 1, 0, _S2, _pol(_S2, 2 * math.pi / 5)),
+    (1, 3, 0, _S3, _pol(_S3, -2 * math.pi / 3)),
+    (1, 2, 0, 0.1, 0.1),
+    (1, 2, 1, 0.1, complex(-0.1, 1e-7)),
+    (2, 0, 0, _S1, _pol(_S1, math.pi / 5)),
+    (6, 0, 0, _S1, _pol(_S1, -math.pi / 5)),
+    (4, 0, 0, 0.5, -0.5),
+)
+
+
+def designed_tile_pair(entries=RELIABILITY_TILE, hp=8, wp=8, D=2, channel_map=None, scale=1.0):
+    """Two real tiles [hp, wp, D] (float64) whose orthonormal 2-D real DFTs (last
+    axis halved) hold `entries` (ky, kx, channel, F_a, F_b) times `scale`.
+    `channel_map` relabels the entries' channels (e.g. {1: 66} puts channel 1's
+    values into channel 66)."""
+    nkx = wp // 2 + 1
+    fa = np.zeros((hp, nkx, D), dtype=np.complex128)
+    fb = np.zeros((hp, nkx, D), dtype=np.complex128)
+    cmap = channel_map or {}
+    for ky, kx, c, va, vb in entries:
+        c = cmap.get(c, c)
+        fa[ky, kx, c] = va * scale
+        fb[ky, kx, c] = vb * scale
+    for f in (fa, fb):
+        for kx in range(nkx):
+            if kx == 0 or (wp % 2 == 0 and kx == wp // 2):
+                for ky in range(hp):
+                    assert abs(f[(-ky) % hp, kx] - np.conj(f[ky, kx])).max() < 1e-15, (ky, kx)
+    ta = np.fft.irfft2(fa, s=(hp, wp), axes=(0, 1), norm="ortho")
+    tb = np.fft.irfft2(fb, s=(hp, wp), axes=(0, 1), norm="ortho")
+    return ta, tb
+
+
+def band_limited_tile(hp, wp, D, rng):
+    """A random real tile whose Nyquist row and column (even edges) are zero in
+    every channel, so those bins of any cross-spectrum vanish."""
+    f = np.fft.rfft2(rng.standard_normal((hp, wp, D)), axes=(0, 1), norm="ortho")
+    if hp % 2 == 0:
+        f[hp // 2] = 0
+    if wp % 2 == 0:
+        f[:, wp // 2] = 0
+    return np.fft.irfft2(f, s=(hp, wp), axes=(0, 1), norm="ortho")
+
+
+def reliability_frames(D=70, seed=5):
+    """A 3-frame [3, 16, 24, D] float64 residual stack with anchors {0, 2} and
+    skipped frame 1 (zero), laid out as 2 x 3 tiles of 8x8:
+      (0,0) the designed tile (channel 1 of the entries moved to channel D-4,
+            so the cancelling pair spans two 64-channel blocks);
+      (0,1) zero in both anchors;
+      (0,2) zero in anchor 0, random in anchor 2;
+      (1,0) band-limited random fields (Nyquist row and column zero), anchor 2 a
+            circular shift of anchor 0 plus noise;
+      (1,1) the designed tile at 1e-3 amplitude (the absolute part of the
+            threshold decides there);
+      (1,2) random, anchor 2 a shift of anchor 0 plus noise."""
+    rng = np.random.default_rng(seed)
+    r = np.zeros((3, 16, 24, D))
+    ta, tb = designed_tile_pair(D=D, channel_map={1: D - 4})
+    r[0, 0:8, 0:8], r[2, 0:8, 0:8] = ta, tb
+    r[2, 0:8, 16:24] = rng.standard_normal((8, 8, D))
+    bl = band_limited_tile(8, 8, D, rng)
+    r[0, 8:16, 0:8] = bl
+    r[2, 8:16, 0:8] = np.roll(bl, (1, 2), axis=(0, 1)) + 0.3 * band_limited_tile(8, 8, D, rng)
+    ta, tb = designed_tile_pair(D=D, channel_map={1: D - 4}, scale=1e-3)
+    r[0, 8:16, 8:16], r[2, 8:16, 8:16] = ta, tb
+    x = rng.standard_normal((8, 8, D))
+    r[0, 8:16, 16:24] = x
+    r[2, 8:16, 16:24] = np.roll(x, (2, 1), axis=(0, 1)) + 0.5 * rng.standard_normal((8, 8, D))
+    return r

@@ -385,6 +385,50 @@ def test_par_matrix_like(cast_lib):
     check_par(cast_lib, resid, w.anchors, label="matrix write", debug=True)
 
 
+def test_par_reliability_threshold(cast_lib):
+    """App. A.2's reliability rule and eq:confidence's no-reliable-bin case on the
+    GPU: a designed tile whose bins straddle eta (one at 3x, one at 0.75x, one at
+    0.3x, one where two channels in different 64-channel blocks cancel in Z), the
+    same tile at 1e-3 amplitude (the absolute part of eta decides), a tile that is
+    zero in both anchors, one zero in one anchor, band-limited anchors (Nyquist
+    bins zero) and a plain shifted pair.  theta, g and c_p are compared with the
+    oracle on every bin, and the designed bins with their hand-derived values."""
+    resid = W.reliability_frames(D=70, seed=5)
+    anchors = (0, 2)
+    for (_, _, _, st) in OP.par_stats(resid.astype(np.float32).astype(np.float64), anchors)[anchors]:
+        moved = st.reliable & (st.theta != 0)     # fp32 must not flip a bin across the cut
+        assert not moved.any() or math.pi - np.abs(st.theta[moved]).max() > 1e-3
+    for gm in (0, 1, 2):
+        check_par(cast_lib, resid, anchors, gate_mode=gm, label=f"reliability gate{gm}", debug=True)
+    x0 = np.random.default_rng(8).standard_normal(resid.shape)
+    check_par(cast_lib, resid, anchors, accumulate=True, x0=x0, label="reliability acc")
+    _, _, prm, (th, gt, cf) = run_par(cast_lib, resid, anchors, debug=True)
+    th = th.cpu().numpy()[0]
+    gt = gt.cpu().numpy()[0]
+    cf = cf.cpu().numpy()[0]
+    nb = 5                                           # stored columns of an 8-wide tile
+    pi = math.pi
+    want = {(1, 1): pi / 6, (2, 1): -pi / 4, (2, 0): pi / 5, (6, 0): -pi / 5}
+    for ky in range(8):
+        for kx in range(nb):
+            w_ = want.get((ky, kx), 0.0)
+            assert abs(th[0, ky * nb + kx] - w_) <= 1e-4, ("designed tile", ky, kx, th[0, ky * nb + kx])
+            w_ = pi / 6 if (ky, kx) == (1, 1) else 0.0
+            assert abs(th[4, ky * nb + kx] - w_) <= 1e-4, ("designed tile 1e-3", ky, kx)
+    assert abs(cf[0] - (2 * math.sqrt(3) + 0.25 + 4.8e-5) / (4.25 + 4.8e-5 + 1e-8)) <= 1e-5
+    assert abs(cf[4] - (2 * math.sqrt(3) + 0.25) * 1e-6 / (4.25e-6 + 1e-8)) <= 1e-4
+    # zero in both anchors / in one anchor: no reliable bin, c_p = 0, U = 1, and the
+    # gate is sigma(-tau(nu) / T)
+    for tile in (1, 2):
+        assert cf[tile] == 0.0 and np.all(th[tile] == 0.0), tile
+    _, _, _, nu = OP.bin_tables(8, 8)
+    g0 = 1.0 / (1.0 + np.exp((0.25 + 0.5 * nu ** 2) / 0.1))
+    assert np.abs(gt[1].reshape(8, nb) - g0).max() <= 1e-5
+    # band-limited anchors: the Nyquist row and column carry no transport
+    t3 = th[3].reshape(8, nb)
+    assert np.all(t3[4, :] == 0.0) and np.all(t3[:, 4] == 0.0)
+
+
 def test_par_deterministic(cast_lib):
     w = gen.get(W.MATRIX)
     resid, _, _ = gen.par_inputs(w, seed=1)

@@ -146,6 +146,32 @@ def test_par_mutation_caught(name):
     assert caught, f"no PAR pin catches mutation {name}"
 
 
+# Mistakes in App. A.2's reliability rule, planted by editing tile_stats' source.
+ETA_MUTANTS = {
+    "eta_from_mean_W": ("prm.eta_rel * W.max()", "prm.eta_rel * W.mean()"),
+    "eta_max_without_dc": ("prm.eta_rel * W.max()", "prm.eta_rel * W.ravel()[1:].max()"),
+    "drop_absZ_leg": ("(W > eta) & (np.abs(Z) > eta)", "(W > eta)"),
+    "either_leg": ("(W > eta) & (np.abs(Z) > eta)", "(W > eta) | (np.abs(Z) > eta)"),
+    "drop_eta_abs": ("+ prm.eta_abs", "+ 0.0"),
+    "omega_plus_drops_nyquist": ("omega_plus[0, 0] = False",
+                                 "omega_plus[0, 0] = False; omega_plus[:, 0] &= kind[:, 0] != SELF"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(ETA_MUTANTS))
+def test_reliability_mutation_caught(name):
+    import inspect
+    old, new = ETA_MUTANTS[name]
+    text = inspect.getsource(P.tile_stats)
+    bad = text.replace(old, new)
+    assert bad != text, name
+    ns = dict(P.__dict__)
+    exec(compile(bad, "<mutant>", "exec"), ns)
+    mod = clone(P, tile_stats=ns["tile_stats"])
+    caught = _any_pin_fails(mod, TP.PINS)
+    assert caught, f"no PAR pin catches mutation {name}"
+
+
 def test_composition_mutations_caught():
     cases = TP.load_composition_golden()
     for fn in (_composition_clip, _composition_wrong_pair):

@@ -351,11 +351,47 @@ def pin_sites_linear_g0(mod=P):
         assert np.allclose(two[a], x0[a] + s[a], rtol=0, atol=1e-14)
 
 
+def pin_reliability_threshold(mod=P):
+    """App. A.2 worked by hand on a designed 8x8 tile (gen.workloads.RELIABILITY_TILE).
+    max W = 4 (at DC) gives eta = 4e-6 + 1e-8.  Reliable: DC, (1,1) with
+    Z = 1 + e^{i pi/3} (theta pi/6), (2,1) at W = 1.2e-5 (theta -pi/4), the column-0
+    representative (2,0) (theta pi/5) and its mirror (6,0) (-pi/5), and the
+    self-conjugate Nyquist point (4,0) (U = 1).  Unreliable: (3,1) (W = 3e-6 < eta),
+    (1,3) (W = 1.2e-6) and (1,2), whose W = 0.02 passes but whose two channels
+    cancel in Z down to 1e-8.  eq:confidence over the reliable non-DC bins:
+        c = (2 sqrt(3) + 2(1.2e-5) + 1.2e-5 + 1.2e-5 + 0.25)
+            / (2(2) + 2(1.2e-5) + 1.2e-5 + 1.2e-5 + 0.25 + 1e-8).
+    At 1e-3 amplitude every W shrinks by 1e-6, eta = 4e-12 + 1e-8 is set by its
+    absolute part, and only DC, (1,1) and (4,0) stay reliable:
+        c = (2 sqrt(3) + 0.25) 1e-6 / (4.25e-6 + 1e-8)."""
+    from gen.workloads import designed_tile_pair
+    pi = math.pi
+    cases = [
+        (1.0, 4e-6 + 1e-8,
+         {(0, 0): 0.0, (1, 1): pi / 6, (2, 1): -pi / 4, (2, 0): pi / 5, (6, 0): -pi / 5,
+          (4, 0): 0.0},
+         (2 * math.sqrt(3) + 0.25 + 4.8e-5) / (4.25 + 4.8e-5 + 1e-8)),
+        (1e-3, 4e-12 + 1e-8, {(0, 0): 0.0, (1, 1): pi / 6, (4, 0): 0.0},
+         (2 * math.sqrt(3) + 0.25) * 1e-6 / (4.25e-6 + 1e-8)),
+    ]
+    for scale, eta, rel_theta, conf in cases:
+        ta, tb = designed_tile_pair(scale=scale)
+        s = mod.tile_stats(mod.rfft2_ortho(ta), mod.rfft2_ortho(tb), 8, 8, mod.ParParams())
+        assert abs(s.eta - eta) <= 1e-9 * eta, (scale, s.eta, eta)
+        got = {(int(a), int(b)) for a, b in np.argwhere(s.reliable)}
+        assert got == set(rel_theta), (scale, sorted(got))
+        for ky in range(8):
+            for kx in range(5):
+                want = rel_theta.get((ky, kx), 0.0)
+                assert abs(s.theta[ky, kx] - want) <= 1e-9, (scale, ky, kx, s.theta[ky, kx], want)
+        assert abs(s.conf - conf) <= 1e-12, (scale, s.conf, conf)
+
+
 PINS = [pin_dft_bruteforce, pin_dft_numpy, pin_parseval_kappa, pin_round_trip, pin_bin_kinds,
         pin_nu_isotropy, pin_linear_g0, pin_translation_ramp, pin_endpoints, pin_real_valued,
         pin_confidence_bounds, pin_confidence_full_spectrum, pin_coherence_levels,
         pin_no_reliable_bin, pin_swap_symmetry, pin_channel_permutation, pin_gate_shape,
-        pin_wrap, pin_anchor_update, pin_sites_linear_g0]
+        pin_wrap, pin_anchor_update, pin_sites_linear_g0, pin_reliability_threshold]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
