@@ -34,7 +34,8 @@
  *            cast_last_error_detail() gives a thread-local human-readable reason
  *            for the last non-OK status of the calling thread.
  * Threads.   Calls are re-entrant; the library holds no global mutable state other
- *            than the thread-local error detail.
+ *            than the thread-local error detail and the per-GPU static scratch of
+ *            cast_par_reconstruct_noalloc (see there).
  * Determinism. Results are bit-identical from run to run for identical inputs
  *            (fixed-order reductions, no floating-point atomics).
  */
@@ -294,6 +295,30 @@ cast_status_t cast_par_reconstruct(const float* resid, const int* anchors, int n
                                    float* theta_out, float* gate_out, float* conf_out,
                                    void* workspace, size_t workspace_bytes,
                                    hipStream_t stream);
+
+/*
+ * cast_par_reconstruct for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same operation, arguments and results, with the scratch space taken from a
+ * static array the library holds on each GPU (CAST_PAR_STATIC_SCRATCH_BYTES, 16
+ * MiB, kept until the process ends) instead of a caller workspace.  The call
+ * allocates and frees nothing; its device address is looked up once per device on
+ * the first call made with that device current.
+ * Sizes whose cast_par_workspace_bytes exceeds cast_par_static_scratch_bytes()
+ * return CAST_ERR_WORKSPACE (enqueueing nothing).  Every call on one GPU shares
+ * that GPU's array and overwrites it before reading it: calls that overlap on one
+ * GPU (two streams, or two host threads without ordering) race and must be
+ * serialised by the caller.
+ */
+#define CAST_PAR_STATIC_SCRATCH_BYTES (16u << 20)
+cast_status_t cast_par_reconstruct_noalloc(const float* resid, const int* anchors, int n_anchor,
+                                           int n_frames, int Hg, int Wg, int D,
+                                           const cast_par_params_t* params, float* out,
+                                           float* theta_out, float* gate_out, float* conf_out,
+                                           hipStream_t stream);
+
+/* Bytes of the static scratch of cast_par_reconstruct_noalloc on each GPU. */
+size_t cast_par_static_scratch_bytes(void);
 
 /* ------------------------------------------------------------------------
  * Control-aware frame selection (Sec. 3.1 eq:sensitivity; Sec. 4.2 eq:debt,

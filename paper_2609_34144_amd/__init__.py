@@ -25,6 +25,7 @@ EXPORTED = ["cast_status_string", "cast_last_error_detail", "cast_abi_version",
             "cast_route_kv_workspace_bytes", "cast_route_kv", "cast_anchor_attn_workspace_bytes",
             "cast_anchor_attn",
             "cast_par_params_default", "cast_par_workspace_bytes", "cast_par_reconstruct",
+            "cast_par_reconstruct_noalloc", "cast_par_static_scratch_bytes",
             "cast_coupled_params_default", "cast_wo_gram", "cast_route_coupled_workspace_bytes",
             "cast_route_coupled", "cast_select_params_default",
             "cast_frame_select_workspace_bytes", "cast_frame_select", "cast_diag_params_default",
@@ -101,6 +102,11 @@ def load(path: str = LIB_PATH):
     lib.cast_par_reconstruct.restype = _i
     lib.cast_par_reconstruct.argtypes = [_vp, _c.POINTER(_i), _i, _i, _i, _i, _i,
                                          _c.POINTER(ParParams), _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.cast_par_reconstruct_noalloc.restype = _i
+    lib.cast_par_reconstruct_noalloc.argtypes = [_vp, _c.POINTER(_i), _i, _i, _i, _i, _i,
+                                                 _c.POINTER(ParParams), _vp, _vp, _vp, _vp, _vp]
+    lib.cast_par_static_scratch_bytes.restype = _sz
+    lib.cast_par_static_scratch_bytes.argtypes = []
     lib.cast_coupled_params_default.restype = None
     lib.cast_coupled_params_default.argtypes = [_c.POINTER(CoupledParams)]
     lib.cast_wo_gram.restype = _i
@@ -390,6 +396,26 @@ def cast_par_reconstruct(resid, anchors, params: ParParams | None = None, out=No
                                     _ptr(gate_out), _ptr(conf_out), _ptr(ws), wsb,
                                     _stream(stream)))
     return out
+
+
+def cast_par_reconstruct_noalloc(resid, anchors, params: ParParams | None = None, out=None,
+                                 theta_out=None, gate_out=None, conf_out=None, stream=None):
+    """cast_par_reconstruct with the library's static per-GPU scratch instead of a
+    workspace (no device allocation in the call; `out` must be given)."""
+    lib = load()
+    if params is None:
+        params = cast_par_params_default()
+    n_frames, Hg, Wg, D = resid.shape
+    anc = [int(a) for a in anchors]
+    arr = (ctypes.c_int * max(len(anc), 1))(*anc)
+    _check(lib.cast_par_reconstruct_noalloc(_ptr(resid), arr, len(anc), n_frames, Hg, Wg, D,
+                                            ctypes.byref(params), _ptr(out), _ptr(theta_out),
+                                            _ptr(gate_out), _ptr(conf_out), _stream(stream)))
+    return out
+
+
+def cast_par_static_scratch_bytes() -> int:
+    return load().cast_par_static_scratch_bytes()
 
 
 def par_debug_shapes(n_anchor, Hg, Wg, params: ParParams):

@@ -6,6 +6,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "cast_common.h"
 
 namespace cast {
@@ -37,6 +39,34 @@ static cast_status_t check_ws(void* ws, size_t have, size_t need) {
 }
 
 static bool dh_ok(int dh) { return dh == 32 || dh == 64 || dh == 128; }
+
+// Scratch of cast_par_reconstruct_noalloc: one copy per GPU the library runs on,
+// held until the process ends.  In host code `scratch` names a host-side stand-in,
+// not device memory: kernels get the device address that hipGetSymbolAddress
+// returns for the current device, looked up once per device and kept.
+constexpr size_t kParStaticScratchBytes = CAST_PAR_STATIC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kParStaticScratchBytes];
+
+static cast_status_t static_scratch_ptr(void** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* ptrs[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(CAST_ERR_HIP, "par (static scratch): hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(CAST_ERR_UNSUPPORTED, "par (static scratch): device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(mu);
+  if (ptrs[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return fail(CAST_ERR_HIP, "par (static scratch): hipGetSymbolAddress: %s", hipGetErrorString(e));
+    ptrs[dev] = p;
+  }
+  *out = ptrs[dev];
+  return CAST_OK;
+}
 
 }  // namespace cast
 
@@ -273,12 +303,17 @@ size_t cast_par_workspace_bytes(int n_frames, int n_anchor, int Hg, int Wg, int 
   return plan_par(n_frames, n_anchor, Hg, Wg, D, *params).total;
 }
 
-cast_status_t cast_par_reconstruct(const float* resid, const int* anchors, int n_anchor,
-                                   int n_frames, int Hg, int Wg, int D,
-                                   const cast_par_params_t* params, float* out,
-                                   float* theta_out, float* gate_out, float* conf_out,
-                                   void* workspace, size_t workspace_bytes,
-                                   hipStream_t stream) {
+}  // extern "C"
+
+// The validation and dispatch of cast_par_reconstruct.  With `static_scratch`
+// the workspace is this device's static scratch array (found on first use) and
+// a plan larger than it is rejected.
+static cast_status_t par_reconstruct(const float* resid, const int* anchors, int n_anchor,
+                                     int n_frames, int Hg, int Wg, int D,
+                                     const cast_par_params_t* params, float* out,
+                                     float* theta_out, float* gate_out, float* conf_out,
+                                     void* workspace, size_t workspace_bytes, bool static_scratch,
+                                     hipStream_t stream) {
   if (anchors == nullptr) return fail(CAST_ERR_NULL, "par: anchors is NULL");
   cast_status_t st = par_shape_check(n_frames, n_anchor, Hg, Wg, D, params);
   if (st != CAST_OK) return st;
@@ -303,11 +338,44 @@ cast_status_t cast_par_reconstruct(const float* resid, const int* anchors, int n
   if (bypass)
     return launch_par_anchor_update(resid, anchors, n_anchor, Hg, Wg, D, params->accumulate, out, stream);
   ParPlan plan = plan_par(n_frames, n_anchor, Hg, Wg, D, *params);
+  if (static_scratch) {
+    if (plan.total > kParStaticScratchBytes)
+      return fail(CAST_ERR_WORKSPACE,
+                  "par (static scratch): these sizes need %zu bytes of scratch, the static "
+                  "scratch holds %zu; use cast_par_reconstruct with a workspace",
+                  plan.total, kParStaticScratchBytes);
+    st = static_scratch_ptr(&workspace);
+    if (st != CAST_OK) return st;
+    workspace_bytes = kParStaticScratchBytes;
+  }
   st = check_ws(workspace, workspace_bytes, plan.total);
   if (st != CAST_OK) return st;
   return launch_par(resid, anchors, n_anchor, n_frames, Hg, Wg, D, *params, out, theta_out,
                     gate_out, conf_out, plan, workspace, stream);
 }
+
+extern "C" {
+
+cast_status_t cast_par_reconstruct(const float* resid, const int* anchors, int n_anchor,
+                                   int n_frames, int Hg, int Wg, int D,
+                                   const cast_par_params_t* params, float* out,
+                                   float* theta_out, float* gate_out, float* conf_out,
+                                   void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream) {
+  return par_reconstruct(resid, anchors, n_anchor, n_frames, Hg, Wg, D, params, out, theta_out,
+                         gate_out, conf_out, workspace, workspace_bytes, false, stream);
+}
+
+cast_status_t cast_par_reconstruct_noalloc(const float* resid, const int* anchors, int n_anchor,
+                                           int n_frames, int Hg, int Wg, int D,
+                                           const cast_par_params_t* params, float* out,
+                                           float* theta_out, float* gate_out, float* conf_out,
+                                           hipStream_t stream) {
+  return par_reconstruct(resid, anchors, n_anchor, n_frames, Hg, Wg, D, params, out, theta_out,
+                         gate_out, conf_out, nullptr, 0, true, stream);
+}
+
+size_t cast_par_static_scratch_bytes(void) { return kParStaticScratchBytes; }
 
 // ---------------------------------------------------------------------------
 // Control-aware frame selection

@@ -155,6 +155,26 @@ def test_par_validation(lib):
                                     None, None, None, 0, None) == NULL
 
 
+def test_par_noalloc_validation(lib):
+    """The static-scratch variant validates like cast_par_reconstruct and rejects
+    sizes whose scratch exceeds the static array before touching the device."""
+    p = cast.cast_par_params_default()
+    cap = lib.cast_par_static_scratch_bytes()
+    assert cap == 16 << 20
+    arr = (ctypes.c_int * 2)(0, 3)
+    assert lib.cast_par_reconstruct_noalloc(None, arr, 2, 4, 8, 8, 64, ctypes.byref(p), 2 * A,
+                                            None, None, None, None) == NULL
+    arr2 = (ctypes.c_int * 2)(3, 0)
+    assert lib.cast_par_reconstruct_noalloc(A, arr2, 2, 4, 8, 8, 64, ctypes.byref(p), 2 * A,
+                                            None, None, None, None) == ANCHORS
+    # 4096 frames of 64x64 tokens x 4096 channels: far more scratch than the array holds
+    need = lib.cast_par_workspace_bytes(4096, 2, 64, 64, 4096, ctypes.byref(p))
+    assert need > cap
+    big = (ctypes.c_int * 2)(0, 4095)
+    assert lib.cast_par_reconstruct_noalloc(A, big, 2, 4096, 64, 64, 4096, ctypes.byref(p),
+                                            2 * A, None, None, None, None) == WORKSPACE
+    assert "static scratch" in lib.cast_last_error_detail().decode()
+
 def test_par_block_update_validation(lib):
     """update_anchors writes anchor slots of out while anchors of resid are read:
     out must not overlap resid; flags are 0 or 1; the bypass then needs buffers."""
