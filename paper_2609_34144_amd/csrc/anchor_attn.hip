@@ -61,6 +61,8 @@ constexpr int kMaxKeff = kAttnMaxKeff;   // routed chunk indices cached in LDS
 // it by more than this (log2 units): probabilities stay <= 2^8, harmless in fp32
 // sums and bf16 operands, and the O rescale is skipped for most tiles.
 constexpr float kMaxSlack = 8.0f;
+// the lane sum of a tile's 32 probabilities up to which the running max may stay
+constexpr float kSumBound = 256.0f;   // 2^kMaxSlack
 
 struct AttnArgs {
   const uint16_t* q;
@@ -398,9 +400,15 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
     });
   };
 
-  // ---- softmax phase of tile j: mask, row max (one exchange with the other
-  //      half-wave), exponentials packed to the bf16 P^T operands and summed,
-  //      running sum, O rescale when the running max moved
+  // ---- softmax phase of tile j: mask, exponentials against the running max,
+  //      packed to the bf16 P^T operands and summed, running sum.  Every
+  //      probability is at most the lane's sum of 32, so a sum <= 2^kMaxSlack
+  //      (false for inf / NaN) shows that the running max may stay: no tile max
+  //      is needed.  Otherwise (first tile, or a score more than kMaxSlack above
+  //      the running max, or many close to it) the wave takes the exact path: row
+  //      max (one exchange with the other half-wave), the running max moved only
+  //      when the tile max exceeds it by more than kMaxSlack, exponentials again,
+  //      and the O rescale.
   auto softmax_phase = [&](int j) __attribute__((always_inline)) {
     if (tb + j == a.nt_all - 1 && a.L != a.nt_all * kBK) {
       const int key0 = (tb + j) * kBK;
@@ -412,37 +420,48 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
           if (key >= a.L) sn[kb][e] = -INFINITY;
         }
     }
-    float pm = max3f(sn[0][0], sn[0][1], sn[0][2]);
-#pragma unroll
-    for (int k = 1; k < 15; ++k) {
-      const int v = 2 * k + 1;
-      pm = max3f(pm, sn[v / 16][v % 16], sn[(v + 1) / 16][(v + 1) % 16]);
-    }
-    pm = fmaxf(pm, sn[1][15]);
-    // the max used for the exponentials moves only by more than kMaxSlack
-    const u32x2 sw = __builtin_bit_cast(
-        u32x2, __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, pm),
-                                                __builtin_bit_cast(unsigned, pm), false, false));
-    const float mx = fmaxf(__builtin_bit_cast(float, sw.x), __builtin_bit_cast(float, sw.y));
-    const float m_cand = fmaxf(m_run, mx * a.sl2);
-    const bool up = m_cand > m_run + kMaxSlack;
-    const float m_new = up ? m_cand : m_run;
-    const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
     // row sum in fp32 over four partial sums (short dependency chains)
     float pe[32], rs4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int e = 0; e < 32; ++e) {
-      pe[e] = __builtin_amdgcn_exp2f(fmaf(sn[e / 16][e % 16], a.sl2, -m_new));
+      pe[e] = __builtin_amdgcn_exp2f(fmaf(sn[e / 16][e % 16], a.sl2, -m_run));
       rs4[e % 4] += pe[e];
+    }
+    float rs = (rs4[0] + rs4[1]) + (rs4[2] + rs4[3]);
+    if (__ballot(!(rs <= kSumBound)) != 0ull) {
+      float pm = max3f(sn[0][0], sn[0][1], sn[0][2]);
+#pragma unroll
+      for (int k = 1; k < 15; ++k) {
+        const int v = 2 * k + 1;
+        pm = max3f(pm, sn[v / 16][v % 16], sn[(v + 1) / 16][(v + 1) % 16]);
+      }
+      pm = fmaxf(pm, sn[1][15]);
+      const u32x2 sw = __builtin_bit_cast(
+          u32x2, __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, pm),
+                                                  __builtin_bit_cast(unsigned, pm), false, false));
+      const float mx = fmaxf(__builtin_bit_cast(float, sw.x), __builtin_bit_cast(float, sw.y));
+      const float m_cand = fmaxf(m_run, mx * a.sl2);
+      const bool up = m_cand > m_run + kMaxSlack;
+      const float m_new = up ? m_cand : m_run;
+      const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) rs4[g] = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 32; ++e) {
+        pe[e] = __builtin_amdgcn_exp2f(fmaf(sn[e / 16][e % 16], a.sl2, -m_new));
+        rs4[e % 4] += pe[e];
+      }
+      rs = (rs4[0] + rs4[1]) + (rs4[2] + rs4[3]);
+      l_run *= corr;
+      m_run = m_new;
+      if (__ballot(up) != 0ull) {
+#pragma unroll
+        for (int db = 0; db < ND; ++db) acc_o[db] *= corr;
+      }
     }
 #pragma unroll
     for (int g = 0; g < 4; ++g) pp[g / 2][g % 2] = pack8(&pe[8 * g]);
-    l_run = l_run * corr + ((rs4[0] + rs4[1]) + (rs4[2] + rs4[3]));
-    m_run = m_new;
-    if (__ballot(up) != 0ull) {
-#pragma unroll
-      for (int db = 0; db < ND; ++db) acc_o[db] *= corr;
-    }
+    l_run += rs;
   };
 
   // ---- prologue: K[0]; tile -1 has P = 0 and a zeroed V buffer (P = 0 must not

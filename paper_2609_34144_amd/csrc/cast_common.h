@@ -30,23 +30,21 @@ __device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w &
 // ---------------------------------------------------------------------------
 struct RoutePlan {
   int D;            // H * dh
-  int ngrp;         // channel groups of kPoolChannels
-  int spq, tq;      // splits per anchor frame, tokens per split
-  int spk, tk;      // splits per history chunk, tokens per split
-  int items;        // n_a * spq + M * spk
-  size_t off_partial, off_means, off_scores, total;
+  int ngrp;         // channel groups of kMeansCh
+  int segs;         // n_a + M pooled rows
+  size_t off_means, total;
 };
-constexpr int kPoolThreads = 64;
-constexpr int kPoolChannels = kPoolThreads * 8;   // 8 bf16 channels per thread
-constexpr int kRouteMaxM = 4096;   // bitonic keys live in 32 KB of LDS
+constexpr int kMeansWaves = 8;      // waves per pooled-mean block
+constexpr int kMeansCh = 128;       // channels per pooled-mean block (16 lanes x 8 bf16)
+constexpr int kRankMaxM = 256;      // TopK by counting larger keys up to this many chunks
+constexpr int kRouteMaxM = 4096;    // bitonic keys live in 32 KB of LDS
 
 RoutePlan plan_route(int n_a, int S, int H, int dh, int M, int Bv);
 
 // Pooled means of n_a frames of q (S tokens) and M chunks of k (Bv tokens):
 // means [n_a + M, D] fp32 (q_bar rows first).  n_a may be 0.
 cast_status_t launch_pool_means(const void* q, const void* k, int n_a, int S, int M, int Bv,
-                                const RoutePlan& p, float* partial, float* means,
-                                hipStream_t stream);
+                                const RoutePlan& p, float* means, hipStream_t stream);
 
 cast_status_t launch_route(const void* q, const void* k, int n_a, int S, int H, int dh, int M,
                            int Bv, int k_eff, float scale, float* scores_out, int32_t* idx_out,
@@ -60,7 +58,7 @@ constexpr int kCoupledMaxMask = 32768;   // n_a * M retain flags held in LDS by 
 
 struct CoupledPlan {
   RoutePlan qk, v;      // pooled-mean scans of (Q, K) and of V
-  size_t off_partial, off_means_qk, off_means_v, off_u, total;
+  size_t off_means_qk, off_means_v, off_u, total;
 };
 CoupledPlan plan_coupled(int n_a, int S, int H, int dh, int M, int Bv);
 

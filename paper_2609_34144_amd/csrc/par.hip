@@ -23,7 +23,10 @@
 // (Hp, Wp) in [1,8]^2 has its own fully unrolled code path.  With the default
 // 8x8 tiling each pass is one launch over all tile classes (interior, right
 // column, bottom row, corner; kernels in par_fused.hip), so small edge classes do
-// not each pay a launch and a drain; other tilings launch per class.
+// not each pay a launch and a drain; other tilings launch per class.  The fused
+// launches are 1-D grids that give each XCD a contiguous part of each pair's
+// (tile, channel block) range (fused_block_work), so the waves of one XCD sweep
+// neighbouring tiles of the same frames.
 #include "par_device.h"
 
 namespace cast {
@@ -328,7 +331,7 @@ cast_status_t launch_par(const float* resid, const int* anchors, int n_anchor, i
     cs.end[3] = cs.end[2] + (hr > 0 && wr > 0 ? 1 : 0);
     const FusedRow& row = fused_row(hr > 0 ? hr : 8);
     const int wi = (wr > 0 ? wr : 8) - 1;
-    dim3 grid(cs.end[3], pl.n_chblk, pl.n_pairs);
+    const dim3 grid((unsigned)cs.end[3] * pl.n_chblk * pl.n_pairs);
     hipLaunchKernelGGL(row.xspec[wi], grid, dim3(kChb), 0, stream, a, cs, resid, partial);
     st = check_launch("par_xspec");
     if (st != CAST_OK) return st;

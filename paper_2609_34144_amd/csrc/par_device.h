@@ -416,14 +416,31 @@ __device__ __forceinline__ void for_class(const ParArgs& a, const ClassSet& cs, 
   if constexpr (HR < 8 && WR < 8) f(std::integral_constant<int, HR>{}, std::integral_constant<int, WR>{}, class_tile(a, cs.k[3], b - cs.end[2]));
 }
 
+// The fused launches run a 1-D grid of ntiles * n_chblk * n_pairs blocks, pairs one
+// after another.  Block b runs on XCD b % 8; within one pair's range the blocks of
+// one XCD take a contiguous run of the work in the order tile (fastest), channel
+// block, so each XCD sweeps its own part of the frames.
+__device__ __forceinline__ void fused_block_work(int b, int ntiles, int n_chblk,
+                                                 int& tile_b, int& chb, int& pair) {
+  const int per = ntiles * n_chblk;
+  pair = b / per;
+  const int idx = b - pair * per;
+  const int x = idx & 7, j = idx >> 3;
+  const int q = per >> 3, r = per & 7;
+  const int w = x * q + min(x, r) + j;
+  tile_b = w % ntiles;
+  chb = w / ntiles;
+}
+
 template <int HR, int WR>
 __global__ __launch_bounds__(64) void par_xspec_fused(ParArgs a, ClassSet cs,
                                                        const float* __restrict__ resid,
                                                        float* __restrict__ partial) {
   __shared__ float lds[kChb * kXsStride];
-  for_class<HR, WR>(a, cs, blockIdx.x, [&](auto hp, auto wp, int tile) {
-    xspec_block<decltype(hp)::value, decltype(wp)::value>(a, tile, blockIdx.y, blockIdx.z, resid,
-                                                          partial, lds);
+  int tile_b, chb, pair;
+  fused_block_work(blockIdx.x, cs.end[3], a.n_chblk, tile_b, chb, pair);
+  for_class<HR, WR>(a, cs, tile_b, [&](auto hp, auto wp, int tile) {
+    xspec_block<decltype(hp)::value, decltype(wp)::value>(a, tile, chb, pair, resid, partial, lds);
   });
 }
 
@@ -433,9 +450,11 @@ __global__ __launch_bounds__(64) void par_recon_fused(ParArgs a, ClassSet cs,
                                                        float* __restrict__ out,
                                                        const float4* __restrict__ coef) {
   __shared__ float fb_lds[2 * kBins * kChb];
-  for_class<HR, WR>(a, cs, blockIdx.x, [&](auto hp, auto wp, int tile) {
-    recon_block<decltype(hp)::value, decltype(wp)::value, ACC>(a, tile, blockIdx.y, blockIdx.z,
-                                                              resid, out, coef, fb_lds);
+  int tile_b, chb, pair;
+  fused_block_work(blockIdx.x, cs.end[3], a.n_chblk, tile_b, chb, pair);
+  for_class<HR, WR>(a, cs, tile_b, [&](auto hp, auto wp, int tile) {
+    recon_block<decltype(hp)::value, decltype(wp)::value, ACC>(a, tile, chb, pair, resid, out, coef,
+                                                              fb_lds);
   });
 }
 

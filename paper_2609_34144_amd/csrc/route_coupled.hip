@@ -2,7 +2,7 @@
 // eq:omission, eq:abc, eq:risk, eq:objective, eq:topk; App. B eq:abcclosed,
 // eq:boundarycoeff, eq:gain, eq:boundarygain, Algorithm 1).
 //
-// route_pool / route_finalize (route_kv.hip)   token means of Q and K, then of V
+// route_means (route_kv.hip)   token means of Q and K, then of V
 // coupled_omission  grid (anchor x head, range of 16 blocks): scores over the M
 //                   blocks, softmax, o_bar, then for each block of the range
 //                   u = (pi/(1-pi+eps))^2 d^T G_h d with d = o_bar - v_bar[m]
@@ -422,9 +422,7 @@ CoupledPlan plan_coupled(int n_a, int S, int H, int dh, int M, int Bv) {
   p.qk = plan_route(n_a, S, H, dh, M, Bv);
   p.v = plan_route(0, S, H, dh, M, Bv);
   const size_t D = (size_t)H * dh;
-  const size_t partial = (size_t)(p.qk.items > p.v.items ? p.qk.items : p.v.items) * D * sizeof(float);
-  p.off_partial = 0;
-  p.off_means_qk = align_up(partial);
+  p.off_means_qk = 0;
   p.off_means_v = p.off_means_qk + align_up((size_t)(n_a + M) * D * sizeof(float));
   p.off_u = p.off_means_v + align_up((size_t)M * D * sizeof(float));
   p.total = p.off_u + align_up((size_t)n_a * H * M * sizeof(float));
@@ -437,7 +435,6 @@ cast_status_t launch_coupled(const void* q, const void* k, const void* v, const 
                              float* u_out, int32_t* idx_out, const CoupledPlan& p, void* ws,
                              hipStream_t stream) {
   char* base = static_cast<char*>(ws);
-  float* partial = reinterpret_cast<float*>(base + p.off_partial);
   CoupledArgs a{};
   a.means_qk = reinterpret_cast<float*>(base + p.off_means_qk);
   a.means_v = reinterpret_cast<float*>(base + p.off_means_v);
@@ -458,10 +455,10 @@ cast_status_t launch_coupled(const void* q, const void* k, const void* v, const 
   a.tol = prm.tol;
   a.eps = prm.eps;
   for (int j = 0; j < n_a; ++j) a.anchors[j] = (short)anchors[j];
-  cast_status_t st = launch_pool_means(q, k, n_a, S, M, Bv, p.qk, partial,
+  cast_status_t st = launch_pool_means(q, k, n_a, S, M, Bv, p.qk,
                                        const_cast<float*>(a.means_qk), stream);
   if (st != CAST_OK) return st;
-  st = launch_pool_means(v, v, 0, S, M, Bv, p.v, partial, const_cast<float*>(a.means_v), stream);
+  st = launch_pool_means(v, v, 0, S, M, Bv, p.v, const_cast<float*>(a.means_v), stream);
   if (st != CAST_OK) return st;
   const dim3 grid(n_a * H, (M + kOmM - 1) / kOmM);
   const size_t shm = (size_t)(M + 2 * dh + kThreads + kOmM * dh) * sizeof(float);
