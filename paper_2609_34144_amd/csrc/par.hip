@@ -6,10 +6,11 @@
 //              writes its per-bin products F_b conj(F_a) and |F_b||F_a|; the 64
 //              lanes are summed through LDS in fixed lane order into one partial
 //              per (pair, tile, channel block).                        (eq:cross)
-//   par_gate   grid (tile, pair, chunk of kGateTargets targets): one lane per
-//              stored bin sums the partials in fixed order, then computes eta,
+//   par_gate   grid (tile, pair, chunk of kGateTargets targets), four waves: one
+//              lane per stored bin; each wave sums a quarter of the channel blocks'
+//              partials, wave 0 adds the four in wave order, then computes eta,
 //              reliability, theta (representative / mirror / self-conjugate), c_p,
-//              nu, g, and the blend coefficients of the chunk's targets
+//              nu, g; the waves share the blend coefficients of the chunk's targets
 //              A_t = (1-alpha) e^{i g alpha theta} / (Hp Wp) and
 //              B_t = alpha e^{-i g (1-alpha) theta} / (Hp Wp).
 //                                              (App. A.2, eq:confidence, eq:gate)
@@ -39,7 +40,7 @@ template <int HP, int WP>
 __global__ __launch_bounds__(64) void par_xspec_kernel(ParArgs a, TileClass k,
                                                         const float* __restrict__ resid,
                                                         float* __restrict__ partial) {
-  __shared__ float lds[kChb * kXsStride];
+  __shared__ __attribute__((aligned(16))) float lds[kBins * kXsStride];
   xspec_block<HP, WP>(a, class_tile(a, k, blockIdx.x), blockIdx.y, blockIdx.z, resid, partial, lds);
 }
 
@@ -63,12 +64,16 @@ __device__ __forceinline__ float wrap_arg(float y, float x) {
 }
 
 constexpr int kGateTargets = 8;   // targets per gate block
+constexpr int kGateWaves = 4;     // waves per gate block
 
-__global__ __launch_bounds__(64) void par_gate_kernel(ParArgs a, const float* __restrict__ partial,
-                                                       float4* __restrict__ coef) {
+__global__ __launch_bounds__(64 * kGateWaves) void par_gate_kernel(ParArgs a,
+                                                                    const float* __restrict__ partial,
+                                                                    float4* __restrict__ coef) {
+  __shared__ float part[kGateWaves][3][64];
+  __shared__ float2 tg[64];
   const int tile = blockIdx.x, pair = blockIdx.y;
   const TileGeom g = tile_geom(a, tile);
-  const int b = threadIdx.x;
+  const int wv = threadIdx.x >> 6, b = threadIdx.x & 63;
   const int ky = b / kNkx, kx = b - (b / kNkx) * kNkx;
   const int H = g.hp, W = g.wp;
   const bool active = b < kBins && ky < H && kx <= W / 2;
@@ -80,58 +85,80 @@ __global__ __launch_bounds__(64) void par_gate_kernel(ParArgs a, const float* __
     if (mky == ky) kind = 2;
     else if (2 * ky > H) { kind = 1; sky = mky; }
   }
-  float zr = 0.0f, zi = 0.0f, w = 0.0f;
-  if (active) {
-    const float* src = partial + ((long long)pair * a.n_tiles + tile) * a.n_chblk * kVals +
-                       (sky * kNkx + kx) * 3;
-#pragma unroll 8
-    for (int j = 0; j < a.n_chblk; ++j) {
-      zr += src[(long long)j * kVals + 0];
-      zi += src[(long long)j * kVals + 1];
-      w += src[(long long)j * kVals + 2];
+  // wave wv sums its quarter of the channel blocks' partials, in block order
+  {
+    float zr = 0.0f, zi = 0.0f, w = 0.0f;
+    if (active) {
+      const float* src = partial + ((long long)pair * a.n_tiles + tile) * a.n_chblk * kVals +
+                         (sky * kNkx + kx) * 3;
+      const int j0 = a.n_chblk * wv / kGateWaves, j1 = a.n_chblk * (wv + 1) / kGateWaves;
+#pragma unroll 4
+      for (int j = j0; j < j1; ++j) {
+        zr += src[(long long)j * kVals + 0];
+        zi += src[(long long)j * kVals + 1];
+        w += src[(long long)j * kVals + 2];
+      }
     }
-    const float nrm = 1.0f / (float)(H * W);   // orthonormal scaling of both spectra
-    zr *= nrm;
-    zi *= nrm;
-    w *= nrm;
-    if (kind == 1) zi = -zi;                    // mirror = conjugate of its representative
+    part[wv][0][b] = zr;
+    part[wv][1][b] = zi;
+    part[wv][2][b] = w;
   }
-  const float wmax = wave_max(active ? w : 0.0f);
-  const float eta = a.eta_rel * wmax + a.eta_abs;
-  const float zabs = sqrtf(zr * zr + zi * zi);
-  const bool rel = active && (w > eta) && (zabs > eta);
-  float theta = 0.0f;
-  if (rel && kind == 0) theta = wrap_arg(zi, zr);
-  if (rel && kind == 1) theta = -wrap_arg(-zi, zr);
-  const bool omega_plus = rel && !(ky == 0 && kx == 0);
-  const float kappa = hc ? 1.0f : 2.0f;
-  const float num = wave_sum(omega_plus ? kappa * zabs : 0.0f);
-  const float den = wave_sum(omega_plus ? kappa * w : 0.0f);
-  const int n_plus = __popcll(__ballot(omega_plus));
-  const float conf = n_plus > 0 ? num / (den + a.eps) : 0.0f;
-  // nu: physical radius of the bin over the largest stored radius of the tile
-  const int kys = (2 * ky <= H) ? ky : ky - H;
-  const float fy = (float)kys / (float)H, fx = (float)kx / (float)W;
-  const float my = (float)(H / 2) / (float)H, mx = (float)(W / 2) / (float)W;
-  const float rmax = sqrtf(my * my + mx * mx);
-  const float nu = rmax > 0.0f ? sqrtf(fy * fy + fx * fx) / rmax : 0.0f;
-  float gate;
-  if (a.gate_mode == 1) gate = 1.0f;
-  else if (a.gate_mode == 2) gate = 0.0f;
-  else {
-    const float tau = a.tau_low + (a.tau_high - a.tau_low) * powf(nu, a.q);
-    gate = 1.0f / (1.0f + expf(-(conf - tau) / a.T));
+  __syncthreads();
+  if (wv == 0) {
+    float zr = 0.0f, zi = 0.0f, w = 0.0f;
+    if (active) {
+#pragma unroll
+      for (int q = 0; q < kGateWaves; ++q) {
+        zr += part[q][0][b];
+        zi += part[q][1][b];
+        w += part[q][2][b];
+      }
+      const float nrm = 1.0f / (float)(H * W);   // orthonormal scaling of both spectra
+      zr *= nrm;
+      zi *= nrm;
+      w *= nrm;
+      if (kind == 1) zi = -zi;                    // mirror = conjugate of its representative
+    }
+    const float wmax = wave_max(active ? w : 0.0f);
+    const float eta = a.eta_rel * wmax + a.eta_abs;
+    const float zabs = sqrtf(zr * zr + zi * zi);
+    const bool rel = active && (w > eta) && (zabs > eta);
+    float theta = 0.0f;
+    if (rel && kind == 0) theta = wrap_arg(zi, zr);
+    if (rel && kind == 1) theta = -wrap_arg(-zi, zr);
+    const bool omega_plus = rel && !(ky == 0 && kx == 0);
+    const float kappa = hc ? 1.0f : 2.0f;
+    const float num = wave_sum(omega_plus ? kappa * zabs : 0.0f);
+    const float den = wave_sum(omega_plus ? kappa * w : 0.0f);
+    const int n_plus = __popcll(__ballot(omega_plus));
+    const float conf = n_plus > 0 ? num / (den + a.eps) : 0.0f;
+    // nu: physical radius of the bin over the largest stored radius of the tile
+    const int kys = (2 * ky <= H) ? ky : ky - H;
+    const float fy = (float)kys / (float)H, fx = (float)kx / (float)W;
+    const float my = (float)(H / 2) / (float)H, mx = (float)(W / 2) / (float)W;
+    const float rmax = sqrtf(my * my + mx * mx);
+    const float nu = rmax > 0.0f ? sqrtf(fy * fy + fx * fx) / rmax : 0.0f;
+    float gate;
+    if (a.gate_mode == 1) gate = 1.0f;
+    else if (a.gate_mode == 2) gate = 0.0f;
+    else {
+      const float tau = a.tau_low + (a.tau_high - a.tau_low) * powf(nu, a.q);
+      gate = 1.0f / (1.0f + expf(-(conf - tau) / a.T));
+    }
+    // optional diagnostics, laid out per the caller's tile_h x (tile_w/2+1) rows
+    // (written by the first target chunk)
+    const int nkx_out = a.tile_w / 2 + 1;
+    if (blockIdx.z == 0 && b < kBins && ky < a.tile_h && kx < nkx_out) {
+      const long long o = ((long long)pair * a.n_tiles + tile) * a.bins_out + ky * nkx_out + kx;
+      if (a.theta_out) a.theta_out[o] = active ? theta : 0.0f;
+      if (a.gate_out) a.gate_out[o] = active ? gate : 0.0f;
+    }
+    if (a.conf_out && b == 0 && blockIdx.z == 0) a.conf_out[(long long)pair * a.n_tiles + tile] = conf;
+    tg[b] = make_float2(theta, gate);
   }
-  // optional diagnostics, laid out per the caller's tile_h x (tile_w/2+1) rows
-  // (written by the first target chunk)
-  const int nkx_out = a.tile_w / 2 + 1;
-  if (blockIdx.z == 0 && b < kBins && ky < a.tile_h && kx < nkx_out) {
-    const long long o = ((long long)pair * a.n_tiles + tile) * a.bins_out + ky * nkx_out + kx;
-    if (a.theta_out) a.theta_out[o] = active ? theta : 0.0f;
-    if (a.gate_out) a.gate_out[o] = active ? gate : 0.0f;
-  }
-  if (a.conf_out && b == 0 && blockIdx.z == 0) a.conf_out[(long long)pair * a.n_tiles + tile] = conf;
+  __syncthreads();
   if (b >= kBins) return;
+  const float theta = tg[b].x, gate = tg[b].y;
   // blend coefficients of this chunk of the pair's targets (eq:block composition):
   // target k of the pair is fa+1+k for the interior, then (first pair) the frames
   // before the first anchor, then (last pair) the frames after the last anchor
@@ -142,7 +169,7 @@ __global__ __launch_bounds__(64) void par_gate_kernel(ParArgs a, const float* __
   const int k0 = blockIdx.z * kGateTargets, k1 = min(k0 + kGateTargets, n_in + n_lo + n_hi);
   const float inv_gap = 1.0f / (float)(fb - fa);
   const float nrm = 1.0f / (float)(H * W);
-  for (int k = k0; k < k1; ++k) {
+  for (int k = k0 + wv; k < k1; k += kGateWaves) {
     const int t = k < n_in ? fa + 1 + k : (k < n_in + n_lo ? k - n_in : fb + 1 + (k - n_in - n_lo));
     const float alpha = (float)(t - fa) * inv_gap;
     float4 cf = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
@@ -335,7 +362,7 @@ cast_status_t launch_par(const float* resid, const int* anchors, int n_anchor, i
     hipLaunchKernelGGL(row.xspec[wi], grid, dim3(kChb), 0, stream, a, cs, resid, partial);
     st = check_launch("par_xspec");
     if (st != CAST_OK) return st;
-    hipLaunchKernelGGL(par_gate_kernel, gate_grid, dim3(64), 0, stream, a,
+    hipLaunchKernelGGL(par_gate_kernel, gate_grid, dim3(64 * kGateWaves), 0, stream, a,
                        (const float*)partial, coef);
     st = check_launch("par_gate");
     if (st != CAST_OK) return st;
@@ -353,7 +380,7 @@ cast_status_t launch_par(const float* resid, const int* anchors, int n_anchor, i
     st = check_launch("par_xspec");
     if (st != CAST_OK) return st;
   }
-  hipLaunchKernelGGL(par_gate_kernel, gate_grid, dim3(64), 0, stream, a,
+  hipLaunchKernelGGL(par_gate_kernel, gate_grid, dim3(64 * kGateWaves), 0, stream, a,
                      (const float*)partial, coef);
   st = check_launch("par_gate");
   if (st != CAST_OK) return st;

@@ -12,8 +12,9 @@ namespace pardev {
 constexpr int kBins = kParBinsMax;     // 40 stored-bin slots: index ky*5 + kx
 constexpr int kNkx = kParNkxMax;       // 5
 constexpr int kVals = kBins * 3;       // (Re Z, Im Z, W) per slot
-constexpr int kXsStride = kBins + 1;   // odd row stride: conflict-free LDS transpose
 constexpr int kChb = 64;               // channels per block (one wave)
+constexpr int kXsStride = kChb + 2;    // LDS row of one bin slot: 64 lane values + pad (8-byte rows)
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 struct ParArgs {
   float* theta_out;
@@ -142,9 +143,9 @@ __device__ __forceinline__ void fwd_tile(const float (&x)[HP][WP], float (&fr)[H
 // One block of the cross-spectrum pass: tile `tile`, channel block `chb`, pair.
 // Every lane transforms both anchors of its channel (all their loads in flight
 // together); the per-bin products Re(F_b conj F_a), Im(F_b conj F_a) and
-// |F_b||F_a| are summed over the 64 lanes through LDS, one quantity at a time (a
-// 64 x 41 transpose, 10.5 KB, so that LDS does not limit the number of resident
-// blocks), in fixed lane order.
+// |F_b||F_a| are summed over the 64 lanes through LDS, one quantity at a time (40
+// rows of 64 lane values plus pad, 10.6 KB, so that LDS does not limit the number
+// of resident blocks), in fixed lane order.
 template <int HP, int WP>
 __device__ __forceinline__ void xspec_block(const ParArgs& a, int tile, int chb, int pair,
                                             const float* __restrict__ resid,
@@ -167,7 +168,6 @@ __device__ __forceinline__ void xspec_block(const ParArgs& a, int tile, int chb,
     fwd_tile<HP, WP>(xb, br, bi);
   }
   const float live = valid ? 1.0f : 0.0f;   // lanes past D contribute nothing
-  float* row = lds + lane * kXsStride;
   float* dst = partial + (((long long)pair * a.n_tiles + tile) * a.n_chblk + chb) * kVals;
   fft::static_for<0, 3>([&](auto qq) {
     constexpr int q = decltype(qq)::value;
@@ -176,25 +176,32 @@ __device__ __forceinline__ void xspec_block(const ParArgs& a, int tile, int chb,
       constexpr int ky = decltype(bb)::value / kNkx;
       constexpr int kx = decltype(bb)::value % kNkx;
       constexpr int s = ky * kNkx + kx;
+      float* cell = lds + s * kXsStride + lane;
       if constexpr (kx < NKX && ky < col_rows(kx, HP, WP)) {
         const float xr = ar[ky][kx], xi = ai[ky][kx], yr = br[ky][kx], yi = bi[ky][kx];
-        if constexpr (q == 0) row[s] = live * (yr * xr + yi * xi);
-        else if constexpr (q == 1) row[s] = self_conj(ky, kx, HP, WP) ? 0.0f : live * (yi * xr - yr * xi);
-        else row[s] = live * sqrtf((xr * xr + xi * xi) * (yr * yr + yi * yi));
+        if constexpr (q == 0) *cell = live * (yr * xr + yi * xi);
+        else if constexpr (q == 1) *cell = self_conj(ky, kx, HP, WP) ? 0.0f : live * (yi * xr - yr * xi);
+        else *cell = live * sqrtf((xr * xr + xi * xi) * (yr * yr + yi * yi));
       } else {
-        row[s] = 0.0f;
+        *cell = 0.0f;
       }
     });
-    for (int s = HP * kNkx; s < kBins; ++s) row[s] = 0.0f;
+    for (int s = HP * kNkx; s < kBins; ++s) lds[s * kXsStride + lane] = 0.0f;
     __syncthreads();
     if (lane < kBins) {
+      // slot `lane`'s 64 lane values are one contiguous row: 8-byte reads, all in
+      // flight together; partial sum g takes the lanes l = g mod 4 in order
+      const f32x2* rowp = reinterpret_cast<const f32x2*>(lds + lane * kXsStride);
+      f32x2 v[kChb / 2];
+#pragma unroll
+      for (int k = 0; k < kChb / 2; ++k) v[k] = rowp[k];
       float s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
-#pragma unroll 16
-      for (int l = 0; l < kChb; l += 4) {
-        s0 += lds[(l + 0) * kXsStride + lane];
-        s1 += lds[(l + 1) * kXsStride + lane];
-        s2 += lds[(l + 2) * kXsStride + lane];
-        s3 += lds[(l + 3) * kXsStride + lane];
+#pragma unroll
+      for (int k = 0; k < kChb / 2; k += 2) {
+        s0 += v[k].x;
+        s1 += v[k].y;
+        s2 += v[k + 1].x;
+        s3 += v[k + 1].y;
       }
       dst[lane * 3 + q] = (s0 + s1) + (s2 + s3);
     }
@@ -436,7 +443,7 @@ template <int HR, int WR>
 __global__ __launch_bounds__(64) void par_xspec_fused(ParArgs a, ClassSet cs,
                                                        const float* __restrict__ resid,
                                                        float* __restrict__ partial) {
-  __shared__ float lds[kChb * kXsStride];
+  __shared__ __attribute__((aligned(16))) float lds[kBins * kXsStride];
   int tile_b, chb, pair;
   fused_block_work(blockIdx.x, cs.end[3], a.n_chblk, tile_b, chb, pair);
   for_class<HR, WR>(a, cs, tile_b, [&](auto hp, auto wp, int tile) {
