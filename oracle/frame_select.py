@@ -108,6 +108,23 @@ def select_next(deltas, h_prev, anchors_prev, k_f: int, lambda_cov: float = LAMB
     return topk_frames(s, k_f), h, s, rs
 
 
+def scores_exact(deltas, h, k_f: int, lambda_cov: float = LAMBDA_COV, eps: float = EPS):
+    """The plain definition in float64 with no rounding between steps (r, the
+    min-max normalisation, d, D and S of eq:sensitivity, eq:normalization,
+    eq:debt, eq:score), for the ages `h` after the block.  The float32 pipeline
+    above takes its decision in the kernels' precision; this is the reference it
+    is held to."""
+    rs = [None if dl is None else response_rms(dl) for dl in deltas]
+    n_cur = len(h)
+    norms = []
+    for r in rs:
+        if r is not None:
+            norms.append((r - r.min()) / (r.max() - r.min() + eps))
+    d = np.mean(norms, axis=0) if norms else None
+    debt = np.asarray(h, dtype=np.float64) / float(-(-n_cur // k_f))
+    return lambda_cov * debt if d is None else d + lambda_cov * debt
+
+
 def brute_topk(s, k_f: int) -> list[int]:
     """The K_f-subset with the largest score sum and, among equal sums, the
     lexicographically smallest index set (brute force over all subsets)."""

@@ -8,7 +8,9 @@ operations that both sides perform with one rounding each, so they must agree to
 by fp32 scores: exact wherever the oracle's K-th / (K+1)-th score gap exceeds
 1e-5; inside that band the GPU's set must be a valid TopK of its own scores.
 Debt-only selection (no control branch) has exactly representable scores on both
-sides and must match exactly.  Each scheduling run continues from the GPU's
+sides and must match exactly.  The scores are also held to the float64 definition
+(no rounding between steps): within 2e-6, and the anchors exact wherever that
+definition's K-th / (K+1)-th gap exceeds 1e-5.  Each scheduling run continues from the GPU's
 anchors, so both sides stay in lockstep."""
 import numpy as np
 import pytest
@@ -49,6 +51,13 @@ def one_step(cast_lib, cam, act, prev, k_f, ages, h_or, label, n_cur=None, lambd
         g_r = r_out[row].cpu().numpy().astype(np.float64)
         assert np.max(np.abs(g_r - r) / np.maximum(np.abs(r), 1e-30)) <= R_REL, (label, row)
     assert np.max(np.abs(g_s - s_or)) <= S_ABS, (label, np.max(np.abs(g_s - s_or)))
+    # and against the float64 definition: scores within fp32 rounding, the anchors
+    # exact wherever the exact K-th / (K+1)-th gap is clear of it
+    ex = FS.scores_exact([to_np(cam), to_np(act)], h_or, k_f, lambda_cov)
+    assert np.max(np.abs(g_s - ex)) <= 2 * S_ABS, (label, np.max(np.abs(g_s - ex)))
+    srt_ex = np.sort(ex)[::-1]
+    if k_f == n or srt_ex[k_f - 1] - srt_ex[k_f] > GAP:
+        assert g_anchors == sorted(sorted(range(n), key=lambda i: (-ex[i], i))[:k_f]), label
     assert len(g_anchors) == k_f and g_anchors == sorted(set(g_anchors))
     srt = np.sort(s_or.astype(np.float64))[::-1]
     gap = srt[k_f - 1] - srt[k_f] if k_f < n else np.inf

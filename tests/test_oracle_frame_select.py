@@ -119,7 +119,29 @@ def pin_strong_response_wins(mod=FS):
     assert s[5] == max(s) and s[4] == 0.0
 
 
-PINS = [pin_rms_closed_form, pin_normalize, pin_sensitivity_branches, pin_ages_and_hcov,
+def pin_float32_against_exact(mod=FS):
+    """The float32 decision pipeline against the float64 definition (no rounding
+    between steps): scores within fp32 rounding, and the same anchors wherever the
+    exact K-th / (K+1)-th gap is clear of it."""
+    rng = np.random.default_rng(77)
+    for trial in range(40):
+        n_cur = int(rng.integers(2, 12))
+        k_f = int(rng.integers(1, n_cur + 1))
+        cam = rng.standard_normal((n_cur, 6, 5)) * rng.uniform(0.3, 3.0, (n_cur, 1, 1))
+        act = rng.standard_normal((n_cur, 6, 5)) * rng.uniform(0.3, 3.0, (n_cur, 1, 1))
+        deltas = [cam, act if trial % 3 else None]
+        h_prev = rng.integers(0, 4, n_cur)
+        prev = sorted(rng.choice(n_cur, size=max(1, n_cur // 2), replace=False).tolist())
+        anchors, h, s32, _ = mod.select_next(deltas, h_prev, prev, k_f)
+        ex = FS.scores_exact(deltas, h, k_f)
+        assert np.max(np.abs(s32.astype(np.float64) - ex)) <= 1e-6, trial
+        srt = np.sort(ex)[::-1]
+        if k_f == n_cur or srt[k_f - 1] - srt[k_f] > 1e-5:
+            want = sorted(sorted(range(n_cur), key=lambda i: (-ex[i], i))[:k_f])
+            assert anchors == want, (trial, anchors, want)
+
+
+PINS = [pin_float32_against_exact, pin_rms_closed_form, pin_normalize, pin_sensitivity_branches, pin_ages_and_hcov,
         pin_debt_only_interleaves, pin_score_cases, pin_topk_ties_bruteforce,
         pin_strong_response_wins]
 
