@@ -5,15 +5,17 @@ torch's current stream:  cast_route_kv -> cast_anchor_attn -> cast_par_reconstru
 (accumulate mode, X_t += R_hat_t).  Inputs are resident in HBM before timing;
 the step cycles over several copies of its inputs so that consecutive steps do
 not find their inputs in the Infinity Cache.  The timed steps are launched eagerly
-(--graph: replayed from one captured HIP graph per input copy); the per-call
-breakdown is timed eagerly, with events between the calls.
+(--graph: replayed from one captured HIP graph per input copy); then each call is
+timed alone, K launches back to back between one pair of events.
 
 Prints ONE JSON line.  `value` = frame-tokens/s = N_cur * S / step time.
-`roofline` describes the dominant kernel (routed attention: bf16 MFMA); the
-per-call figures for routing and PAR are reported beside it.  `cpu_baseline`
-times the float64 oracle on a bounded sample of the same workload on this host.
+`roofline` describes the dominant call (routed attention: bf16 MFMA; PAR on a
+workload without attention); the per-call figures for routing and PAR are
+reported beside it.  `cpu_baseline` times the float64 oracle on a bounded sample
+of the same workload on this host.  The default workload is the HY-World-like
+block, the largest one that runs all three calls.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--step-only]
 """
 from __future__ import annotations
 
@@ -229,28 +231,18 @@ def main():
 
     ev = lambda: torch.cuda.Event(enable_timing=True)
 
-    def step(s, marks=None):
+    def step(s):
         # launched on the current stream (torch's stream, or the capture stream
         # while a graph is captured)
         st = torch.cuda.current_stream()
-        if marks is not None:
-            marks[0].record(st)
         if w.has_attention:
             _, ke, _ = cast.cast_route_kv(s["q"], s["k"], w.topk, w.scale, idx_out=idx,
                                           workspace=route_ws, stream=st)
-            if marks is not None:
-                marks[1].record(st)
             cast.cast_anchor_attn(s["q"], s["k"], s["v"], idx, ke, w.scale, out=attn_out,
                                   workspace=attn_ws, stream=st)
-        elif marks is not None:
-            marks[1].record(st)
-        if marks is not None:
-            marks[2].record(st)
         if w.has_par:
             cast.cast_par_reconstruct(s["resid"], w.anchors, prm, out=s["x"], workspace=par_ws,
                                       stream=st)
-        if marks is not None:
-            marks[3].record(st)
 
     for i in range(args.warmup):
         step(sets[i % N_COPIES])
