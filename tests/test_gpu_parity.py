@@ -119,6 +119,21 @@ def test_route_ties_and_budget(cast_lib):
     check_route(cast_lib, q, k, 4, 0.3, "ties")
 
 
+@pytest.mark.parametrize("M", [64, 65, 256, 257, 1000])
+def test_route_many_chunks(cast_lib, M):
+    """Chunk counts around the TopK's paths: rank counting (one wave per 64 chunks,
+    up to 256 chunks) and the bitonic sorts above; budgets below, at and above a
+    multiple of 64, with byte-identical duplicate chunks for exact ties."""
+    torch.manual_seed(500 + M)
+    dev = "cuda"
+    n_a, S, H, dh, Bv = 2, 40, 3, 64, 24
+    q = torch.randn(n_a, S, H, dh, device=dev).to(torch.bfloat16)
+    k = torch.randn(M, Bv, H, dh, device=dev).to(torch.bfloat16)
+    k[M - 1] = k[3]                                   # exact tie: chunk 3 must win it
+    k[M // 2] = k[1]
+    for topk in (1, 7, 64, 100):
+        check_route(cast_lib, q, k, topk, 0.125, f"M{M} k{topk}")
+
 def test_route_deterministic(cast_lib):
     w = gen.get(W.MATRIX)
     q, k, _, _, _ = gen.attn_inputs(w, seed=3, device="cuda")
