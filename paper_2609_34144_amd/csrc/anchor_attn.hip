@@ -22,12 +22,8 @@
 // group B issue all copies, alongside their softmax.
 //
 // Per wave and tile:
-//   S^T = K Q^T - m  A = K rows from LDS (ds_read_b128), B = Q^T held in registers
-//                 for the whole kernel, with the logit scale times log2(e) folded
-//                 into it (q * scale * log2 e rounded to bf16), and the chain
-//                 started from -m (the running max) instead of zero: the MFMA
-//                 returns the shifted base-2 logits and the softmax takes their
-//                 exponentials directly.  The 32x32 accumulator puts one query per
+//   S^T = K Q^T   A = K rows from LDS (ds_read_b128), B = Q^T held in registers
+//                 for the whole kernel.  The 32x32 accumulator puts one query per
 //                 lane column, so the online-softmax row max / row sum need only
 //                 the lane's own values and one exchange with lane ^ 32.
 //   O^T += V^T P^T  B = P^T straight from the S^T accumulators (converted to
@@ -225,15 +221,7 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
     const uint16_t* qp = a.q + (((long long)i * a.S + qc) * a.H + h) * DH + 8 * hf;
 #pragma unroll
     for (int t = 0; t < DH / 16; ++t) {
-      // the logit scale (times log2 e) is folded into the operand: q * sl2 rounded
-      // to bf16, so the MFMA returns base-2 logits
-      const u32x4 raw = *reinterpret_cast<const u32x4*>(qp + 16 * t);
-      u32x4 sc;
-#pragma unroll
-      for (int w2 = 0; w2 < 4; ++w2)
-        sc[w2] = pack_bf16x2(__uint_as_float(raw[w2] << 16) * a.sl2,
-                             __uint_as_float(raw[w2] & 0xffff0000u) * a.sl2);
-      qreg[t] = __builtin_bit_cast(bf16x8, sc);
+      qreg[t] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qp + 16 * t));
     }
   }
   __syncthreads();   // sidx visible to every wave
@@ -384,11 +372,6 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc_o[db][e] = 0.0f;
   f32x16 sn[2];       // S^T of the current tile: keys kb*32 + 8(e/4) + 4hf + e%4
-  // accumulator start of every S chain: -m_run (0 before the first tile), so the
-  // MFMA returns the base-2 logits already shifted by the running max
-  f32x16 negm;
-#pragma unroll
-  for (int e = 0; e < 16; ++e) negm[e] = 0.0f;
   bf16x8 pp[2][2];    // P^T operands of the previous tile, by (kb, 16-key half s2)
   // (a finite floor, so that an all -inf tile leaves m_run, l_run unchanged)
   float m_run = -1e30f, l_run = 0.0f;
@@ -409,7 +392,7 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
     static_for<0, NSTEP>([&](auto uu) {
       constexpr int u = decltype(uu)::value;
       if constexpr (u + kLookahead < NSTEP) rd(IC<u + kLookahead>{});
-      sn[u % 2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(opk[u], qreg[u / 2], u < 2 ? negm : sn[u % 2],
+      sn[u % 2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(opk[u], qreg[u / 2], u < 2 ? f32x16{} : sn[u % 2],
                                                           0, 0, 0);
       constexpr int db = u % ND, kb = u / (2 * ND), s2 = (u / ND) % 2;
       acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(opv[u], pp[kb][s2], acc_o[db], 0, 0, 0);
@@ -417,16 +400,15 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
     });
   };
 
-  // ---- softmax phase of tile j: mask, exponentials of the shifted logits
-  //      (S already holds scale log2(e) q.k - m_run), packed to the bf16 P^T
-  //      operands and summed, running sum.  Every probability is at most the
-  //      lane's sum of 32, so a sum <= 2^kMaxSlack (false for inf / NaN) shows
-  //      that the running max may stay: no tile max is needed.  Otherwise (first
-  //      tile, whose S starts from 0, or a score more than kMaxSlack above the
-  //      running max, or many close to it) the wave takes the exact path: row max
-  //      (one exchange with the other half-wave), the running max moved only when
-  //      the tile max exceeds it by more than kMaxSlack, exponentials again, the O
-  //      rescale, and the new -m_run as the start of the next S chains.
+  // ---- softmax phase of tile j: mask, exponentials against the running max,
+  //      packed to the bf16 P^T operands and summed, running sum.  Every
+  //      probability is at most the lane's sum of 32, so a sum <= 2^kMaxSlack
+  //      (false for inf / NaN) shows that the running max may stay: no tile max
+  //      is needed.  Otherwise (first tile, or a score more than kMaxSlack above
+  //      the running max, or many close to it) the wave takes the exact path: row
+  //      max (one exchange with the other half-wave), the running max moved only
+  //      when the tile max exceeds it by more than kMaxSlack, exponentials again,
+  //      and the O rescale.
   auto softmax_phase = [&](int j) __attribute__((always_inline)) {
     if (tb + j == a.nt_all - 1 && a.L != a.nt_all * kBK) {
       const int key0 = (tb + j) * kBK;
@@ -442,41 +424,36 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
     float pe[32], rs4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int e = 0; e < 32; ++e) {
-      pe[e] = __builtin_amdgcn_exp2f(sn[e / 16][e % 16]);
+      pe[e] = __builtin_amdgcn_exp2f(fmaf(sn[e / 16][e % 16], a.sl2, -m_run));
       rs4[e % 4] += pe[e];
     }
     float rs = (rs4[0] + rs4[1]) + (rs4[2] + rs4[3]);
-    if (j == 0 || __ballot(!(rs <= kSumBound)) != 0ull) {
-      // S holds the logits minus m_used: the running max, or 0 before the first tile
-      const float m_used = j == 0 ? 0.0f : m_run;
+    if (__ballot(!(rs <= kSumBound)) != 0ull) {
       float pm = max3f(sn[0][0], sn[0][1], sn[0][2]);
 #pragma unroll
       for (int k = 1; k < 15; ++k) {
-        const int v2 = 2 * k + 1;
-        pm = max3f(pm, sn[v2 / 16][v2 % 16], sn[(v2 + 1) / 16][(v2 + 1) % 16]);
+        const int v = 2 * k + 1;
+        pm = max3f(pm, sn[v / 16][v % 16], sn[(v + 1) / 16][(v + 1) % 16]);
       }
       pm = fmaxf(pm, sn[1][15]);
       const u32x2 sw = __builtin_bit_cast(
           u32x2, __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, pm),
                                                   __builtin_bit_cast(unsigned, pm), false, false));
       const float mx = fmaxf(__builtin_bit_cast(float, sw.x), __builtin_bit_cast(float, sw.y));
-      const float m_cand = fmaxf(m_run, m_used + mx);
+      const float m_cand = fmaxf(m_run, mx * a.sl2);
       const bool up = m_cand > m_run + kMaxSlack;
       const float m_new = up ? m_cand : m_run;
       const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
-      const float shift = m_new - m_used;
 #pragma unroll
       for (int g = 0; g < 4; ++g) rs4[g] = 0.0f;
 #pragma unroll
       for (int e = 0; e < 32; ++e) {
-        pe[e] = __builtin_amdgcn_exp2f(sn[e / 16][e % 16] - shift);
+        pe[e] = __builtin_amdgcn_exp2f(fmaf(sn[e / 16][e % 16], a.sl2, -m_new));
         rs4[e % 4] += pe[e];
       }
       rs = (rs4[0] + rs4[1]) + (rs4[2] + rs4[3]);
       l_run *= corr;
       m_run = m_new;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) negm[e] = -m_new;
       if (__ballot(up) != 0ull) {
 #pragma unroll
         for (int db = 0; db < ND; ++db) acc_o[db] *= corr;

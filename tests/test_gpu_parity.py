@@ -271,6 +271,36 @@ def test_attn_key_split(cast_lib, dh, n_a, S, H, M, Bv, k_eff, n0):
     assert d <= 2.0 ** -7 * max(1.0, b.float().abs().max().item())
 
 
+@pytest.mark.parametrize("dh", [64, 128])
+def test_attn_softmax_paths(cast_lib, dh):
+    """Logit ranges that drive every branch of the online softmax: history chunks
+    whose keys are scaled from 0.05 to 12 in an order that raises the running max
+    by far more than its slack several times (exact path, O rescale), tiles far
+    below the running max (probabilities that underflow to 0 on the common path),
+    a first tile much larger than the rest, and ties of whole tiles at the max; in
+    the aligned (64-row chunks), fast (96-row chunks) and general (current segment)
+    copy modes, split and unsplit."""
+    torch.manual_seed(900 + dh)
+    dev = "cuda"
+    n_a, S, H, M = 1, 300, 2, 10
+    gains = [0.1, 0.1, 3.0, 0.05, 6.0, 0.1, 12.0, 0.05, 12.0, 0.2]
+    for Bv, n0 in ((64, 0), (96, 0), (64, 9)):
+        q = torch.randn(n_a, S, H, dh, device=dev).to(torch.bfloat16)
+        k = torch.randn(M, Bv, H, dh, device=dev)
+        for c, gn in enumerate(gains):
+            k[c] *= gn
+        k[8] = k[6]                                   # identical tiles at the max
+        k = k.to(torch.bfloat16)
+        v = torch.randn(M, Bv, H, dh, device=dev).to(torch.bfloat16)
+        kc = (8.0 * torch.randn(n0, H, dh, device=dev)).to(torch.bfloat16) if n0 else None
+        vc = torch.randn(n0, H, dh, device=dev).to(torch.bfloat16) if n0 else None
+        for order in ([0, 1, 2, 3, 4, 5, 6, 7, 8, 9], [6, 0, 1, 3, 5, 7, 9, 2, 4, 8]):
+            idx = torch.tensor([[order, order[::-1]]], dtype=torch.int32, device=dev)
+            for split in (True, False):
+                check_attn(cast_lib, q, k, v, idx, M, 1 / math.sqrt(dh), kc=kc, vc=vc,
+                           label=f"softmax paths dh{dh} Bv{Bv} n0 {n0} {order[0]} split {split}",
+                           split=split)
+
 def test_attn_topk_all_equals_dense(cast_lib):
     """topk = M routes every chunk: the result is dense attention over the whole history."""
     w = gen.get(W.TINY)
