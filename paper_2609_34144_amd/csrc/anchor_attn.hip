@@ -18,8 +18,8 @@
 // (buffer_load_dwordx4 ... lds), so no registers or VALU work stage it.  Each
 // lane of a copy instruction picks its source row and 16-byte chunk, which lets
 // the LDS image be XOR-swizzled against bank conflicts even though the copy
-// writes 1 KB contiguously.  Two K and two V buffers rotate; the four waves of
-// group B issue all copies, alongside their softmax.
+// writes 1 KB contiguously.  Two K and two V buffers rotate; group A copies the
+// K tiles and group B the V tiles, each at the start of its softmax interval.
 //
 // Per wave and tile:
 //   S^T = K Q^T   A = K rows from LDS (ds_read_b128), B = Q^T held in registers
@@ -56,6 +56,8 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kBQ = kWaves * 32;   // queries per workgroup: one block of 32 per wave
 // operand reads issued this many MFMA steps ahead of their use
 constexpr int kLookahead = 3;
+// s_waitcnt vmcnt(0) that leaves expcnt and lgkmcnt free
+constexpr int kVmcntBase = 0x0F70;
 constexpr int kMaxKeff = kAttnMaxKeff;   // routed chunk indices cached in LDS
 // The running max used for the exponentials moves only when the tile max exceeds
 // it by more than this (log2 units): probabilities stay <= 2^8, harmless in fp32
@@ -236,8 +238,8 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
 
   const unsigned row_bytes = (unsigned)(a.H * DH * 2), head_bytes = (unsigned)(h * DH * 2);
 
-  // ---- copy slots.  The four waves of group B copy every tile: wave 4 + w takes
-  //      K (and V) slots k = w + 4r, r < KSL / 4.  Slot k fills LDS chunks
+  // ---- copy slots.  The four waves of a group share the copy of a tile: wave
+  //      w (mod 4) takes slots k = w + 4r, r < KSL / 4.  Slot k fills LDS chunks
   //      ci = 64 k + lane of its tile: row ci / CPR = brow + r RSTEP with
   //      brow = w 512/DH + lane / CPR, physical chunk lane % CPR, which holds logical
   //      chunk (lane % CPR) ^ swz(row).  Both swizzles depend on the row only
@@ -319,21 +321,23 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
       }
     });
   };
-  Cursor cur_k{}, cur_v{};
-  if constexpr (FAST) {
-    cur_k = cursor_at(tb + min(1, nt - 1));
-    cur_v = cursor_at(tb);
-  }
-  // copies(c): K[c + 1] and V[c] (those that exist; c counts from tile tb)
-  auto issue_copies = [&](int c, uint16_t* kdst, uint16_t* vdst) __attribute__((always_inline)) {
+  // Copies of the tiles of j+1, at the start of the softmax interval of tile j:
+  // group A copies K[j+1] (interval 2j+1), group B copies V[j+1] (interval
+  // 2j+2), each into the buffer of tile j-1, and each waits for its copies at
+  // the end of that interval.  Issuing a tile's copies holds the issuing waves
+  // for about 16 cycles per 1-KB copy (the buffer unit's rate); split between
+  // the groups, neither softmax interval grows past the MFMA phase beside it.
+  // Both groups walk tiles j+1 = 1, 2, ... with one cursor per wave.
+  Cursor cur{};
+  if constexpr (FAST) cur = cursor_at(tb + min(1, nt - 1));
+  auto own_copies = [&](int j, uint16_t* kdst, uint16_t* vdst) __attribute__((always_inline)) {
+    if (j + 1 < nt) {
+      const TileMap m = FAST ? cur_map(cur) : TileMap{};
+      if (grp == 0) copy_tile(IC<0>{}, tb + j + 1, m, kdst);
+      else copy_tile(IC<1>{}, tb + j + 1, m, vdst);
+    }
     if constexpr (FAST) {
-      if (c + 1 < nt) copy_tile(IC<0>{}, tb + c + 1, cur_map(cur_k), kdst);
-      if (c < nt) copy_tile(IC<1>{}, tb + c, cur_map(cur_v), vdst);
-      if (c + 2 < nt) advance(cur_k);
-      if (c + 1 < nt) advance(cur_v);
-    } else {
-      if (c + 1 < nt) copy_tile(IC<0>{}, tb + c + 1, TileMap{}, kdst);
-      if (c < nt) copy_tile(IC<1>{}, tb + c, TileMap{}, vdst);
+      if (j + 2 < nt) advance(cur);
     }
   };
 
@@ -474,33 +478,34 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
     u32x4* z = reinterpret_cast<u32x4*>(lds_v1);
     for (int x = tid; x < kBK * DH / 8; x += kThreads) z[x] = u32x4{0u, 0u, 0u, 0u};
   }
-  if (grp == 1) {
-    if constexpr (FAST) copy_tile(IC<0>{}, tb, cur_map(cursor_at(tb)), lds_k0);
-    else copy_tile(IC<0>{}, tb, TileMap{}, lds_k0);
+  {
+    const TileMap m0 = FAST ? cur_map(cursor_at(tb)) : TileMap{};
+    if (grp == 0) copy_tile(IC<0>{}, tb, m0, lds_k0);
+    else copy_tile(IC<1>{}, tb, m0, lds_v0);
   }
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   // Group B runs one interval behind group A.  Interval 2j: A does the MFMAs of
   // tile j while B does the softmax of tile j-1; interval 2j+1: A the softmax of
-  // tile j, B the MFMAs of tile j.  B copies K[j+1] and V[j] at the start of
-  // interval 2j (with its softmax, which is shorter than the MFMA phase running
-  // beside it) and waits for them at the end of interval 2j+1.
-  if (grp == 1) {
-    issue_copies(0, lds_k1, lds_v0);
-    __syncthreads();
-  }
+  // tile j, B the MFMAs of tile j.  A copies K[j+1] at the start of interval
+  // 2j+1, B copies V[j+1] at the start of interval 2j+2, each into a buffer that
+  // no MFMA phase reads in that interval.
+  if (grp == 1) __syncthreads();
   // One tile per call; K[j] in K buffer j%2, V[j-1] in V buffer (j-1)%2.  Every
   // call runs the same MFMA phase: at j = 0 it meets tile -1 (P = 0 and a zeroed V
   // buffer), at j = nt it computes a throw-away S from a stale K buffer.
   auto iter = [&](auto par, int j) __attribute__((always_inline)) {
     constexpr int P = decltype(par)::value;
-    uint16_t* const kc = P == 0 ? lds_k0 : lds_k1;   // K[j]; then K[j+2]
+    uint16_t* const kc = P == 0 ? lds_k0 : lds_k1;   // K[j]
+    uint16_t* const kn = P == 0 ? lds_k1 : lds_k0;   // K[j-1]; then K[j+1]
     uint16_t* const vp = P == 0 ? lds_v1 : lds_v0;   // V[j-1]; then V[j+1]
     if (live) mfma_phase(kc, vp);
-    if (grp == 1) __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (grp == 1) issue_copies(j + 1, kc, vp);
+    own_copies(j, kn, vp);
     if (j < nt && live) softmax_phase(j);
+    // the copies of this interval land before the barrier publishes them (the
+    // barrier's release fence waits too; the same wait in both groups)
+    __builtin_amdgcn_s_waitcnt(kVmcntBase);
     __syncthreads();
   };
   int j = 0;
