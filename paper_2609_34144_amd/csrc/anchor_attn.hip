@@ -424,12 +424,13 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
           if (key >= a.L) sn[kb][e] = -INFINITY;
         }
     }
-    // row sum in fp32 over four partial sums (short dependency chains)
-    float pe[32], rs4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    // row sum in fp32 over four partial sums (short dependency chains), each
+    // started from its first term (not 0 + p: the compiler keeps that add)
+    float pe[32], rs4[4];
 #pragma unroll
     for (int e = 0; e < 32; ++e) {
       pe[e] = __builtin_amdgcn_exp2f(fmaf(sn[e / 16][e % 16], a.sl2, -m_run));
-      rs4[e % 4] += pe[e];
+      rs4[e % 4] = e < 4 ? pe[e] : rs4[e % 4] + pe[e];
     }
     float rs = (rs4[0] + rs4[1]) + (rs4[2] + rs4[3]);
     if (__ballot(!(rs <= kSumBound)) != 0ull) {
@@ -449,11 +450,9 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
       const float m_new = up ? m_cand : m_run;
       const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
 #pragma unroll
-      for (int g = 0; g < 4; ++g) rs4[g] = 0.0f;
-#pragma unroll
       for (int e = 0; e < 32; ++e) {
         pe[e] = __builtin_amdgcn_exp2f(fmaf(sn[e / 16][e % 16], a.sl2, -m_new));
-        rs4[e % 4] += pe[e];
+        rs4[e % 4] = e < 4 ? pe[e] : rs4[e % 4] + pe[e];
       }
       rs = (rs4[0] + rs4[1]) + (rs4[2] + rs4[3]);
       l_run *= corr;

@@ -220,6 +220,30 @@ def test_attn_fast_and_aligned_modes(cast_lib, dh):
                    label=f"modes dh{dh} Bv{Bv}")
 
 
+@pytest.mark.parametrize("dh", [64, 128])
+@pytest.mark.parametrize("Bv,k_eff,n0", [
+    (64, 1, 0), (64, 2, 0), (64, 3, 0),      # aligned mode: 1, 2, 3 key tiles
+    (100, 1, 0), (100, 2, 0), (70, 3, 0),    # fast mode: 2, 4, 4 key tiles, ragged last one
+    (30, 0, 70), (30, 2, 70), (20, 1, 5),    # general mode: 2, 3, 1 key tiles
+])
+def test_attn_short_key_sequences(cast_lib, dh, Bv, k_eff, n0):
+    """Key sequences of one to four 64-key tiles in every copy mode: the tiles that
+    the first copies fill (K[0], V[0] before the loop, K[1], V[1] with tile 0) and
+    the copy cursor held at the last tile."""
+    torch.manual_seed(500 + dh + Bv + k_eff + n0)
+    dev = "cuda"
+    n_a, S, H, M = 2, 140, 2, 4
+    q = torch.randn(n_a, S, H, dh, device=dev).to(torch.bfloat16)
+    k = torch.randn(M, Bv, H, dh, device=dev).to(torch.bfloat16)
+    v = torch.randn(M, Bv, H, dh, device=dev).to(torch.bfloat16)
+    kc = torch.randn(n0, H, dh, device=dev).to(torch.bfloat16) if n0 else None
+    vc = torch.randn(n0, H, dh, device=dev).to(torch.bfloat16) if n0 else None
+    rng = np.random.default_rng(k_eff * 7 + Bv)
+    idx = torch.tensor(rng.integers(0, M, size=(n_a, H, k_eff)), dtype=torch.int32, device=dev)
+    check_attn(cast_lib, q, k, v, idx, k_eff, 1 / math.sqrt(dh), kc=kc, vc=vc,
+               label=f"short dh{dh} Bv{Bv} k{k_eff} n0 {n0}")
+
+
 @pytest.mark.parametrize("Bv,k_eff,n0", [(64, 96, 0), (72, 70, 0), (40, 80, 13)])
 def test_attn_many_routed_chunks(cast_lib, Bv, k_eff, n0):
     """More than 64 routed chunks (the kernel keeps the first 64 chunk indices in a
