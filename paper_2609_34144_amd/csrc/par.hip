@@ -190,8 +190,8 @@ __global__ __launch_bounds__(64) void par_recon_kernel(ParArgs a, TileClass k,
                                                         float* __restrict__ out,
                                                         const float4* __restrict__ coef) {
   __shared__ float fb_lds[2 * kBins * kChb];
-  recon_block<HP, WP, ACC>(a, class_tile(a, k, blockIdx.x), blockIdx.y, blockIdx.z, resid, out,
-                           coef, fb_lds);
+  recon_block<HP, WP, ACC, false>(a, class_tile(a, k, blockIdx.x), blockIdx.y, blockIdx.z, resid,
+                                  out, coef, fb_lds);
 }
 
 // Host-side table of the per-shape kernels, indexed [HP-1][WP-1].
@@ -366,8 +366,10 @@ cast_status_t launch_par(const float* resid, const int* anchors, int n_anchor, i
                        (const float*)partial, coef);
     st = check_launch("par_gate");
     if (st != CAST_OK) return st;
-    hipLaunchKernelGGL(p.accumulate ? row.recon_a[wi] : row.recon_w[wi], grid, dim3(kChb), 0,
-                       stream, a, cs, resid, out, (const float4*)coef);
+    // accumulate mode with several pairs: stream the targets (see recon_body)
+    const ReconFusedFn rf = !p.accumulate ? row.recon_w[wi]
+                            : (pl.n_pairs > 1 ? row.recon_as[wi] : row.recon_a[wi]);
+    hipLaunchKernelGGL(rf, grid, dim3(kChb), 0, stream, a, cs, resid, out, (const float4*)coef);
     return check_launch("par_recon");
   }
   // other tilings: one launch per tile class and pass

@@ -65,8 +65,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t frame_rsrc(const float* base, 
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base) + frame * frame_elems, 0,
                                            (int)(unsigned)(frame_elems * 4), kBufDword3);
 }
+template <int AUX = 0>
 __device__ __forceinline__ float buf_ld(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff) {
-  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0));
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, AUX));
 }
 template <int AUX>
 __device__ __forceinline__ void buf_st(__amdgpu_buffer_rsrc_t r, unsigned voff, unsigned soff,
@@ -228,7 +229,8 @@ constexpr int unique_slot(int ky, int kx) {
 }
 
 // The anchor case of eq:block on one (tile, channel): out[f] = R_f, or += R_f.
-template <int HP, int WP, bool ACC>
+// NTT: the read-modify-write of out streams (nontemporal load and store).
+template <int HP, int WP, bool ACC, bool NTT>
 __device__ __forceinline__ void anchor_tile_update(const ParArgs& a, const float* __restrict__ resid,
                                                    float* __restrict__ out, int f, unsigned tile0,
                                                    unsigned WgD4, unsigned D4, unsigned c4) {
@@ -240,17 +242,21 @@ __device__ __forceinline__ void anchor_tile_update(const ParArgs& a, const float
     fft::static_for<0, WP>([&](auto xx) {
       constexpr int xi = decltype(xx)::value;
       v[xi] = buf_ld(src, c4, tile0 + y * WgD4 + xi * D4);
-      if constexpr (ACC) o[xi] = buf_ld(dst, c4, tile0 + y * WgD4 + xi * D4);
+      if constexpr (ACC) o[xi] = buf_ld<NTT ? kNT : 0>(dst, c4, tile0 + y * WgD4 + xi * D4);
     });
     fft::static_for<0, WP>([&](auto xx) {
       constexpr int xi = decltype(xx)::value;
-      if constexpr (ACC) buf_st<0>(dst, c4, tile0 + y * WgD4 + xi * D4, o[xi] + v[xi]);
+      if constexpr (ACC) buf_st<NTT ? kNT : 0>(dst, c4, tile0 + y * WgD4 + xi * D4, o[xi] + v[xi]);
       else buf_st<kNT>(dst, c4, tile0 + y * WgD4 + xi * D4, v[xi]);
     });
   });
 }
 
-template <int HP, int WP, bool ACC>
+// NTT (accumulate mode): the targets' read-modify-write streams past the caches
+// (nontemporal loads and stores).  With several anchor pairs this pass reads every
+// interior anchor once per adjacent pair, and streaming the targets keeps those
+// anchors in the Infinity Cache for the second read.
+template <int HP, int WP, bool ACC, bool NTT>
 __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __restrict__ resid,
                                            float* __restrict__ out,
                                            const float4* __restrict__ coef, const TileGeom& g,
@@ -267,8 +273,8 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
   if (a.update_anchors) {
     // pair p updates its left anchor, the last pair its right one too, so every
     // anchor slot is written once (out does not overlap resid)
-    anchor_tile_update<HP, WP, ACC>(a, resid, out, fa, tile0, WgD4, D4, c4);
-    if (pair == a.n_anchor - 2) anchor_tile_update<HP, WP, ACC>(a, resid, out, fb, tile0, WgD4, D4, c4);
+    anchor_tile_update<HP, WP, ACC, NTT>(a, resid, out, fa, tile0, WgD4, D4, c4);
+    if (pair == a.n_anchor - 2) anchor_tile_update<HP, WP, ACC, NTT>(a, resid, out, fb, tile0, WgD4, D4, c4);
   }
   float ar[HP][NKX], ai[HP][NKX];
   {
@@ -316,7 +322,7 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
           constexpr int y = decltype(yy)::value;
           fft::static_for<0, WP>([&](auto xx) {
             constexpr int xi = decltype(xx)::value;
-            old[y][xi] = buf_ld(dst, c4, tile0 + y * wgd + xi * dd);
+            old[y][xi] = buf_ld<NTT ? kNT : 0>(dst, c4, tile0 + y * wgd + xi * dd);
           });
         });
       }
@@ -373,7 +379,7 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
         fft::static_for<0, WP>([&](auto xx) {
           constexpr int xi = decltype(xx)::value;
           const unsigned so = tile0 + y * wgd + xi * dd;
-          if constexpr (ACC) buf_st<0>(dst, c4, so, old[y][xi] + xv[xi]);
+          if constexpr (ACC) buf_st<NTT ? kNT : 0>(dst, c4, so, old[y][xi] + xv[xi]);
           else buf_st<kNT>(dst, c4, so, xv[xi]);
         });
       });
@@ -382,12 +388,12 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
 }
 
 // One block of the reconstruction pass: tile `tile`, channel block `chb`, pair.
-template <int HP, int WP, bool ACC>
+template <int HP, int WP, bool ACC, bool NTT>
 __device__ __forceinline__ void recon_block(const ParArgs& a, int tile, int chb, int pair,
                                             const float* __restrict__ resid, float* __restrict__ out,
                                             const float4* __restrict__ coef, float* fb_lds) {
   const TileGeom g = tile_geom(a, tile);
-  recon_body<HP, WP, ACC>(a, resid, out, coef, g, tile, chb * kChb + threadIdx.x, pair,
+  recon_body<HP, WP, ACC, NTT>(a, resid, out, coef, g, tile, chb * kChb + threadIdx.x, pair,
                           fb_lds + threadIdx.x);
 }
 
@@ -451,7 +457,7 @@ __global__ __launch_bounds__(64) void par_xspec_fused(ParArgs a, ClassSet cs,
   });
 }
 
-template <int HR, int WR, bool ACC>
+template <int HR, int WR, bool ACC, bool NTT>
 __global__ __launch_bounds__(64) void par_recon_fused(ParArgs a, ClassSet cs,
                                                        const float* __restrict__ resid,
                                                        float* __restrict__ out,
@@ -460,8 +466,8 @@ __global__ __launch_bounds__(64) void par_recon_fused(ParArgs a, ClassSet cs,
   int tile_b, chb, pair;
   fused_block_work(blockIdx.x, cs.end[3], a.n_chblk, tile_b, chb, pair);
   for_class<HR, WR>(a, cs, tile_b, [&](auto hp, auto wp, int tile) {
-    recon_block<decltype(hp)::value, decltype(wp)::value, ACC>(a, tile, chb, pair, resid, out, coef,
-                                                              fb_lds);
+    recon_block<decltype(hp)::value, decltype(wp)::value, ACC, NTT>(a, tile, chb, pair, resid, out,
+                                                                   coef, fb_lds);
   });
 }
 
@@ -472,7 +478,7 @@ typedef void (*ReconFusedFn)(ParArgs, ClassSet, const float*, float*, const floa
 // (each row is compiled in its own translation unit).
 struct FusedRow {
   XspecFusedFn xspec[8];
-  ReconFusedFn recon_w[8], recon_a[8];
+  ReconFusedFn recon_w[8], recon_a[8], recon_as[8];   // write, accumulate, accumulate streaming
 };
 
 void fused_row_1(FusedRow& r);

@@ -16,8 +16,9 @@ namespace pardev {
 template <int HR, int WR>
 static void set_entry(FusedRow& r) {
   r.xspec[WR - 1] = par_xspec_fused<HR, WR>;
-  r.recon_w[WR - 1] = par_recon_fused<HR, WR, false>;
-  r.recon_a[WR - 1] = par_recon_fused<HR, WR, true>;
+  r.recon_w[WR - 1] = par_recon_fused<HR, WR, false, false>;
+  r.recon_a[WR - 1] = par_recon_fused<HR, WR, true, false>;
+  r.recon_as[WR - 1] = par_recon_fused<HR, WR, true, true>;
 }
 
 void CAST_CAT(fused_row_, CAST_PAR_HR)(FusedRow& r) {
