@@ -20,7 +20,7 @@ eq:gain, eq:boundarygain, Algorithm 1, tab:config routing weights / stopping):
   backward, ...) replace an anchor's mask by TopK(G) when that lowers J by more
   than tol * max(J, 1e-8); a pass with no change stops early.
 
-Readings (listed in the design doc): the optimisation is per head (masks of
+Readings where the paper leaves a choice: the optimisation is per head (masks of
 different heads never interact), so J and its acceptance threshold are the
 head's own; TopK orders (value descending, block index ascending) and reports
 ascending block indices; the omission stabiliser eps is 1e-8 unless given; the

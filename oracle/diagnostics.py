@@ -18,7 +18,7 @@ orthonormal real 2-D DFT, real-FFT multiplicities kappa, normalised radius nu):
 * phase progress of one coefficient: (phi_t - phi_a) / (phi_b - phi_a) on phases
   unwrapped along the frames.
 
-Readings (listed in the design doc): the bands are given by edges on PAR's nu
+Readings where the paper leaves a choice: the bands are given by edges on PAR's nu
 (band k holds edges[k] <= nu < edges[k+1], the last band also nu = 1); the energy
 weight of the phase error is kappa |F_t|^2; eps = 1e-8.
 """

@@ -18,7 +18,7 @@ eq:normalization and the scheduling rules:
   neither endpoint mandatory; a dense block is a block whose anchors are all
   frames (it resets every age).
 
-Readings (listed in DESIGN.md): eps = 1e-8 (the paper's stabiliser elsewhere;
+Readings where the paper leaves a choice: eps = 1e-8 (the paper's stabiliser elsewhere;
 its value is not given here); the decision is taken in float32, the precision
 the kernels compute scores in: r is formed in float64 and rounded to float32,
 every later step is float32 arithmetic with one rounding per operation.

@@ -27,7 +27,7 @@ What it computes, in the paper's order and notation:
   before a_0 use (a_0, a_1) with alpha < 0, frames after a_J use
   (a_{J-1}, a_J) with alpha > 1; alpha is never clipped; K_f >= 2.
 
-Readings where the paper leaves a choice (each is listed in the design doc):
+Readings where the paper leaves a choice:
 forward transform sign exp(-2 pi i k n / N) and the halved axis is the last
 (x / width) axis; Arg is taken in (-pi, pi] (atan2, then -pi -> pi) on
 representatives only; a mirror bin takes the reliability flag and the negated

@@ -9,7 +9,7 @@ chunk score s_{i,m} = q_bar_i . k_bar_m * scale (the paper's scale is
 keeps exactly K_KV = min(topk, M) blocks per anchor (fewer than K_KV blocks:
 keep all and report the realised budget).
 
-Readings (listed in the design doc): routing is per (anchor frame, head); the pooled
+Readings where the paper leaves a choice: routing is per (anchor frame, head); the pooled
 query is the mean over all S tokens of the anchor frame, the pooled key the
 mean over the B_v tokens of the block, so q_bar . k_bar equals the mean of
 q . k over all token pairs; the TopK order is (score descending, chunk index
