@@ -502,8 +502,9 @@ __global__ __launch_bounds__(kThreads, 1) void anchor_attn_kernel(AttnArgs a) {
     __syncthreads();
     own_copies(j, kn, vp);
     if (j < nt && live) softmax_phase(j);
-    // the copies of this interval land before the barrier publishes them (the
-    // barrier's release fence waits too; the same wait in both groups)
+    // the copies of this interval land before the barrier publishes them: an
+    // explicit wait, the same in both groups (the barrier's workgroup fence does
+    // not reliably wait for copies into LDS)
     __builtin_amdgcn_s_waitcnt(kVmcntBase);
     __syncthreads();
   };
