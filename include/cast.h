@@ -26,6 +26,11 @@
  *              K, V    bf16 [M, Bv, H, dh]       (M historical blocks of Bv tokens)
  *              resid   fp32 [n_frames, Hg, Wg, D]
  *            bf16 is IEEE binary32 truncated to its upper 16 bits (as torch.bfloat16).
+ * Alignment. The bf16 tensors of the routing and attention calls (Q, K, V, the
+ *            current segment, the attention output) and W_O / the Gram matrix are
+ *            16-byte aligned; every other fp32 or int32 buffer is 4-byte aligned
+ *            (the bf16 control inputs of cast_frame_select 2-byte aligned).  A
+ *            misaligned buffer gives CAST_ERR_SHAPE.
  * Streams.   Every call only enqueues work on `stream` (NULL = the legacy default
  *            stream) and returns; nothing synchronises the host.  Asynchronous
  *            device faults surface at the caller's next stream synchronisation.

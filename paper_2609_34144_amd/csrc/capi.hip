@@ -124,6 +124,8 @@ cast_status_t cast_route_kv(const void* q, const void* k_hist, int n_a, int S, i
     return fail(CAST_ERR_NULL, "route: q, k_hist and idx_out are required");
   if (!aligned(q, 16) || !aligned(k_hist, 16))
     return fail(CAST_ERR_SHAPE, "route: q and k_hist must be 16-byte aligned");
+  if (!aligned(idx_out, 4) || !aligned(scores_out, 4))
+    return fail(CAST_ERR_SHAPE, "route: idx_out and scores_out must be 4-byte aligned");
   RoutePlan plan = plan_route(n_a, S, H, dh, M, Bv);
   st = check_ws(workspace, workspace_bytes, plan.total);
   if (st != CAST_OK) return st;
@@ -195,6 +197,8 @@ cast_status_t cast_route_coupled(const void* q, const void* k_hist, const void* 
     return fail(CAST_ERR_NULL, "coupled: q, k_hist, v_hist, gram and idx_out are required");
   if (!aligned(q, 16) || !aligned(k_hist, 16) || !aligned(v_hist, 16) || !aligned(gram, 16))
     return fail(CAST_ERR_SHAPE, "coupled: q, k_hist, v_hist, gram must be 16-byte aligned");
+  if (!aligned(idx_out, 4) || !aligned(u_out, 4))
+    return fail(CAST_ERR_SHAPE, "coupled: idx_out and u_out must be 4-byte aligned");
   CoupledPlan plan = plan_coupled(n_a, S, H, dh, M, Bv);
   st = check_ws(workspace, workspace_bytes, plan.total);
   if (st != CAST_OK) return st;
@@ -244,6 +248,8 @@ cast_status_t cast_anchor_attn(const void* q, const void* k_hist, const void* v_
   const void* ptrs[] = {q, k_hist, v_hist, k_cur, v_cur, out};
   for (const void* p : ptrs)
     if (p != nullptr && !aligned(p, 16)) return fail(CAST_ERR_SHAPE, "attn: tensors must be 16-byte aligned");
+  if (!aligned(idx, 4) || !aligned(lse_out, 4))
+    return fail(CAST_ERR_SHAPE, "attn: idx and lse_out must be 4-byte aligned");
   // no workspace: every unit runs whole
   AttnSplitPlan plan{(int)((long long)n_a * H * ((S + 255) / 256)), 0, 1, 0};
   if (workspace != nullptr) {
@@ -327,7 +333,9 @@ static cast_status_t par_reconstruct(const float* resid, const int* anchors, int
   if (bypass && !params->update_anchors) return CAST_OK;
   if (!bypass && n_anchor < 2) return fail(CAST_ERR_ANCHORS, "par: reconstruction needs K_f >= 2 anchors");
   if (resid == nullptr || out == nullptr) return fail(CAST_ERR_NULL, "par: resid and out are required");
-  if (!aligned(resid, 4) || !aligned(out, 4)) return fail(CAST_ERR_SHAPE, "par: misaligned buffers");
+  if (!aligned(resid, 4) || !aligned(out, 4) || !aligned(theta_out, 4) || !aligned(gate_out, 4) ||
+      !aligned(conf_out, 4))
+    return fail(CAST_ERR_SHAPE, "par: misaligned buffers");
   if (params->update_anchors) {
     // anchor slots of out are written while other blocks read the anchors of resid
     const unsigned long long bytes = (unsigned long long)n_frames * Hg * Wg * D * sizeof(float);
