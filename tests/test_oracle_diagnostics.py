@@ -147,9 +147,31 @@ def pin_oracle_corrections(mod=DG):
     assert not np.allclose(rm, ref, atol=1e-3)
 
 
+def pin_frame_diagnostics_translation(mod=DG):
+    """eq:shift and eq:block together: a band-limited field translated by t d per
+    frame, anchors (0, 4), one periodic 16x16 tile per frame.  The cross-spectrum
+    phase is then -w.4d per bin (|w.4d| < pi here), so the transport with the
+    gate forced to 1 reconstructs every skipped frame exactly, interior (alpha =
+    1/4, 1/2, 3/4) and extrapolated (frame 5, alpha = 5/4) alike: the per-frame
+    diagnostics must report e_t = 0, no band energy and no transport phase error
+    for each of them, which holds only if each frame is paired with its own
+    anchors, alpha and theta."""
+    d = np.array([0.05, -0.03])
+    base = _bandlimit(rng(8).standard_normal((16, 16, 3)))
+    ref = np.stack([fourier_shift(base, d * t) for t in range(6)])
+    prm = P.ParParams(tile_h=16, tile_w=16, gate_mode=1)
+    approx = P.par_reconstruct(ref, (0, 4), prm)
+    out = mod.frame_diagnostics(ref, approx, (0, 4), prm, [0.0, 0.5, 1.0])
+    assert sorted(out) == [1, 2, 3, 5]
+    for t, v in out.items():
+        assert v["nrmse"] < 1e-9, (t, v["nrmse"])
+        assert v["phase_err"] < 1e-9, (t, v["phase_err"])
+        assert np.abs(v["bands"]).max() < 1e-9, (t, v["bands"])
+
+
 PINS = [pin_nrmse, pin_band_parseval, pin_band_single_frequency, pin_band_split,
         pin_phase_error_translation,
-        pin_phase_progress, pin_oracle_corrections]
+        pin_phase_progress, pin_oracle_corrections, pin_frame_diagnostics_translation]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])

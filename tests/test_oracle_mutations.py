@@ -415,7 +415,31 @@ def _dg_phase_error_amplitude_weight(ref_t, anchor_a, theta_tiles, alpha, tile_h
     return num / (den + eps)
 
 
+def _dg_frame_diag(anchor_of_pair=0, flip_alpha=False, approx_from_anchor=False):
+    """frame_diagnostics with one assembly mistake planted."""
+    def f(ref, approx, anchors, prm, edges, eps=1e-8):
+        ref = np.asarray(ref, dtype=np.float64)
+        n = ref.shape[0]
+        stats = P.par_stats(ref, anchors, prm)
+        out = {}
+        for (t, a, b, alpha) in P.composition(anchors, n):
+            th = [st.theta for (_, _, _, st) in stats[(a, b)]]
+            anc = ref[b] if anchor_of_pair else ref[a]
+            al = 1.0 - alpha if flip_alpha else alpha
+            ap = approx[a] if approx_from_anchor else approx[t]
+            rp, rm = DG.oracle_corrections(ref[t], ref[a], ref[b], alpha, prm.tile_h, prm.tile_w)
+            out[t] = dict(nrmse=DG.nrmse(ref[t], ap, eps),
+                          bands=DG.band_energy(ref[t], ap, prm.tile_h, prm.tile_w, edges, eps),
+                          phase_err=DG.phase_error(ref[t], anc, th, al, prm.tile_h, prm.tile_w, eps),
+                          r_phase=rp, r_mag=rm)
+        return out
+    return f
+
+
 DG_MUTANTS = {
+    "frame_diag_phase_from_anchor_b": dict(frame_diagnostics=_dg_frame_diag(anchor_of_pair=1)),
+    "frame_diag_alpha_flipped": dict(frame_diagnostics=_dg_frame_diag(flip_alpha=True)),
+    "frame_diag_error_of_anchor": dict(frame_diagnostics=_dg_frame_diag(approx_from_anchor=True)),
     "band_no_kappa": dict(band_energy=_dg_band_no_kappa),
     "nrmse_squared": dict(nrmse=_dg_nrmse_squared),
     "no_unwrap": dict(unwrap_track=_dg_unwrap_none),
