@@ -200,6 +200,46 @@ def test_coupling_hand_example():
     assert [t["row"] for t in trace] == [0, 1, 1, 0]     # forward, then backward
 
 
+def _first_visit(x):
+    """The hand example with u_0[1] = x: gains, improvement, J and decision of
+    Algorithm 1's first row visit (anchor 0)."""
+    u = np.array([[1.0, x, 0.0], [0.0, 0.9, 1.0]])
+    trace = []
+    OC.refine(u, (0, 3), 4, 1, passes=1, trace=trace)
+    t = trace[0]
+    return t["g_new"] - t["g_old"], t["J"], t["accepted"]
+
+
+def test_refine_acceptance_threshold():
+    """Algorithm 1 accepts a row's new set only when its gain improvement exceeds
+    tol * max(J, 1e-8) (tab:config: tol = 1e-6).  u_0[1] is set by bisection so
+    that the improvement is 0.5 or 2 times tol * J (J is about 2.8 here, so the
+    first also exceeds tol itself): rejected, then accepted."""
+    tol = 1e-6
+    for factor, want in ((0.5, False), (2.0, True)):
+        lo, hi = 0.5, 0.6                        # no improvement at 0.5, 0.03 at 0.6
+        for _ in range(80):
+            mid = 0.5 * (lo + hi)
+            d, J, _ = _first_visit(mid)
+            if d > factor * tol * J:
+                hi = mid
+            else:
+                lo = mid
+        d, J, accepted = _first_visit(hi)
+        assert factor * tol * J < d < 1.01 * factor * tol * J
+        assert d > tol                            # an absolute tol would accept both
+        assert accepted == want, (factor, d, J)
+
+
+def test_refine_stops_after_a_pass_without_change():
+    """The hand example changes one row in the first pass and none in the second,
+    so Algorithm 1 ends there however many passes it may take."""
+    u = np.array([[1.0, 0.9, 0.0], [0.0, 0.9, 1.0]])
+    trace = []
+    OC.refine(u, (0, 3), 4, 1, passes=6, trace=trace)
+    assert len(trace) == 4 and [t["accepted"] for t in trace] == [True, False, False, False]
+
+
 def test_route_coupled_shapes_and_bypass():
     """Per-head routing end to end: indices ascending, exactly k_eff per (anchor, head);
     topk >= M keeps every block."""
@@ -250,6 +290,8 @@ def pin_gain_identity(mod):
 def pin_refine(mod):
     _on(mod, test_coupling_hand_example)
     _on(mod, test_refine_descent_budget_termination, 0)
+    _on(mod, test_refine_acceptance_threshold)
+    _on(mod, test_refine_stops_after_a_pass_without_change)
 
 
 PINS = [pin_closed_form, pin_boundary, pin_omission, pin_gain_identity, pin_refine]

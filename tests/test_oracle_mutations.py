@@ -300,19 +300,23 @@ def test_coupled_mutation_caught(name):
 
 
 def test_coupled_refine_mutations_caught():
-    """Accepting ties (no strict decrease) and a forward-only second pass are caught
-    by the hand-worked coupling example's trace."""
-    src = OC.refine.__code__
+    """Mistakes in Algorithm 1's loop: accepting ties (no strict decrease), a
+    forward-only second pass, any positive improvement accepted (no tolerance),
+    the tolerance taken as absolute instead of relative to J, and running every
+    pass after one that changed nothing."""
     import inspect
     text = inspect.getsource(OC.refine)
-    for bad in (text.replace("(g_new - g_old) > tol * max(J, 1e-8)", "(g_new - g_old) >= 0.0"),
-                text.replace("if s % 2 == 0 else range(n_a - 1, -1, -1)", "")):
+    rule = "(g_new - g_old) > tol * max(J, 1e-8)"
+    for bad in (text.replace(rule, "(g_new - g_old) >= 0.0"),
+                text.replace("if s % 2 == 0 else range(n_a - 1, -1, -1)", ""),
+                text.replace(rule, "(g_new - g_old) > 0.0"),
+                text.replace(rule, "(g_new - g_old) > tol"),
+                text.replace("        if not changed:\n            break\n", "")):
         assert bad != text
         ns = dict(OC.__dict__)
         exec(compile(bad, "<mutant>", "exec"), ns)
         mod = clone(OC, refine=ns["refine"])
         assert _any_pin_fails(mod, TC.PINS)
-    del src
 
 
 # ---- control-aware frame selection
