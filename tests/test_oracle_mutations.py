@@ -172,6 +172,30 @@ def test_reliability_mutation_caught(name):
     assert caught, f"no PAR pin catches mutation {name}"
 
 
+# Mistakes in eq:gate (tile_stats) and in the per-head routing loop, planted by
+# editing the functions' source.
+SOURCE_MUTANTS = {
+    "gate_tau_linear_in_nu": (P, "tile_stats", "nu ** prm.q", "nu"),
+    "route_one_head_for_all": (R, "route", "topk_select(sd[i, h], k_eff)", "topk_select(sd[i, 0], k_eff)"),
+    "route_budget_off_by_one": (R, "route", "k_eff = min(int(topk), M)",
+                                "k_eff = int(topk) if int(topk) <= M else M - 1"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SOURCE_MUTANTS))
+def test_source_mutation_caught(name):
+    import inspect
+    mod, fn, old, new = SOURCE_MUTANTS[name]
+    text = inspect.getsource(getattr(mod, fn))
+    bad = text.replace(old, new)
+    assert bad != text, name
+    ns = dict(mod.__dict__)
+    exec(compile(bad, "<mutant>", "exec"), ns)
+    mm = clone(mod, **{fn: ns[fn]})
+    pins = TP.PINS if mod is P else TR.ROUTE_PINS
+    assert _any_pin_fails(mm, pins), f"no pin catches mutation {name}"
+
+
 def test_composition_mutations_caught():
     cases = TP.load_composition_golden()
     for fn in (_composition_clip, _composition_wrong_pair):

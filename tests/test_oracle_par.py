@@ -287,6 +287,10 @@ def pin_gate_shape(mod=P):
     sig = lambda v: 1 / (1 + math.exp(-v))
     assert abs(s.gate[0, 0] - sig((s.conf - 0.25) / 0.1)) < 1e-12
     assert abs(s.gate[4, 4] - sig((s.conf - 0.75) / 0.1)) < 1e-12
+    # an interior radius: bin (2, 2) of an 8x8 tile has nu = |(2/8, 2/8)| / |(1/2, 1/2)|
+    # = 1/2, so tau = 0.25 + 0.5 (1/2)^q = 0.375 with q = 2
+    assert abs(s.nu[2, 2] - 0.5) < 1e-12
+    assert abs(s.gate[2, 2] - sig((s.conf - 0.375) / 0.1)) < 1e-12
     assert sig(2.5) - 1e-9 <= s.gate.min() and s.gate.max() <= sig(7.5) + 1e-9
     # g = 1/2 exactly where c = tau: choose tau_low = c
     prm = mod.ParParams(tau_low=s.conf, tau_high=s.conf + 0.5)

@@ -75,6 +75,28 @@ def pin_route_duplicate_tie(mod=R):
     assert list(idx3[0, 0]) == [0]
 
 
+def pin_route_selection(mod=R):
+    """Every (anchor, head) keeps k_eff = min(topk, M) distinct chunks, listed in
+    ascending order, and each kept chunk outscores each dropped one, with the
+    scores summed by explicit loops over tokens and dims (eq:pooled, eq:topk)."""
+    r = rng(9)
+    n_a, S, H, dh, M, Bv = 3, 4, 3, 5, 7, 3
+    q = r.standard_normal((n_a, S, H, dh))
+    k = r.standard_normal((M, Bv, H, dh))
+    for topk in (2, 7, 9):
+        _, idx, k_eff = mod.route(q, k, topk)
+        assert k_eff == min(topk, M) and idx.shape == (n_a, H, k_eff)
+        for i in range(n_a):
+            for h in range(H):
+                b = [sum(float(q[i, a, h, d] * k[m, c, h, d])
+                         for a in range(S) for c in range(Bv) for d in range(dh)) for m in range(M)]
+                sel = [int(x) for x in idx[i, h]]
+                assert sel == sorted(set(sel)) and len(sel) == k_eff
+                for m in sel:
+                    for n in set(range(M)) - set(sel):
+                        assert b[m] > b[n] or (b[m] == b[n] and m < n), (i, h, m, n)
+
+
 def _sdpa(q, k, v, scale):
     return torch.nn.functional.scaled_dot_product_attention(
         torch.from_numpy(q)[None, None], torch.from_numpy(k)[None, None],
@@ -143,7 +165,8 @@ def pin_attention_rows(mod=A):
         assert abs(Ls[i, h, s] - L[i, h, s]) < 1e-14
 
 
-ROUTE_PINS = [pin_pooled_bruteforce, pin_topk_rules, pin_route_permutation, pin_route_duplicate_tie]
+ROUTE_PINS = [pin_pooled_bruteforce, pin_topk_rules, pin_route_permutation, pin_route_duplicate_tie,
+              pin_route_selection]
 ATTN_PINS = [pin_attention_dense, pin_attention_routed_subset, pin_attention_constant_keys,
              pin_attention_rows]
 
