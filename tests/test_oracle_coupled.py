@@ -7,6 +7,8 @@ retain gains), brute-force single-anchor optimality of TopK(G), strict descent
 and termination of Algorithm 1, and a hand-worked coupling example."""
 from fractions import Fraction
 
+import math
+
 import numpy as np
 import pytest
 
@@ -200,6 +202,21 @@ def test_coupling_hand_example():
     assert [t["row"] for t in trace] == [0, 1, 1, 0]     # forward, then backward
 
 
+def test_pooled_softmax_hand_example():
+    """eq:omission's pooled attention by hand: q_bar = (1, 0) and (0, 2), k_bar =
+    (1, 0) and (0, 1), scale 1/2, so the scores are (1/2, 0) and (0, 1) and
+    pi = (e^(1/2), 1) / (e^(1/2) + 1) and (1, e) / (1 + e); o_bar = pi v_bar."""
+    qb = np.array([[1.0, 0.0], [0.0, 2.0]])
+    kb = np.array([[1.0, 0.0], [0.0, 1.0]])
+    vb = np.array([[3.0, -1.0], [0.5, 2.0]])
+    s, pi, o_bar = OC.pooled_stats(qb, kb, vb, 0.5)
+    e = math.exp(0.5)
+    want = np.array([[e / (e + 1.0), 1.0 / (e + 1.0)], [1.0 / (1.0 + math.e), math.e / (1.0 + math.e)]])
+    assert s == pytest.approx(np.array([[0.5, 0.0], [0.0, 1.0]]), abs=1e-15)
+    assert pi == pytest.approx(want, abs=1e-15)
+    assert o_bar == pytest.approx(want @ vb, abs=1e-14)
+
+
 def _first_visit(x):
     """The hand example with u_0[1] = x: gains, improvement, J and decision of
     Algorithm 1's first row visit (anchor 0)."""
@@ -280,6 +297,7 @@ def pin_boundary(mod):
 def pin_omission(mod):
     _on(mod, test_omission_exact_identity, 0)
     _on(mod, test_omission_projection_norm)
+    _on(mod, test_pooled_softmax_hand_example)
 
 
 def pin_gain_identity(mod):

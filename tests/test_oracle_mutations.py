@@ -179,6 +179,7 @@ SOURCE_MUTANTS = {
     "route_one_head_for_all": (R, "route", "topk_select(sd[i, h], k_eff)", "topk_select(sd[i, 0], k_eff)"),
     "route_budget_off_by_one": (R, "route", "k_eff = min(int(topk), M)",
                                 "k_eff = int(topk) if int(topk) <= M else M - 1"),
+    "coupled_pooled_scores_unscaled": (OC, "pooled_stats", "s = scale * (qb @ kb.T)", "s = (qb @ kb.T)"),
 }
 
 
@@ -192,7 +193,7 @@ def test_source_mutation_caught(name):
     ns = dict(mod.__dict__)
     exec(compile(bad, "<mutant>", "exec"), ns)
     mm = clone(mod, **{fn: ns[fn]})
-    pins = TP.PINS if mod is P else TR.ROUTE_PINS
+    pins = {P: TP.PINS, R: TR.ROUTE_PINS, OC: TC.PINS}[mod]
     assert _any_pin_fails(mm, pins), f"no pin catches mutation {name}"
 
 
