@@ -72,6 +72,18 @@ def pin_band_split(mod=DG):
     assert np.allclose(fr, [e_lo / (e_lo + e_hi), e_hi / (e_lo + e_hi)], rtol=0, atol=1e-12), fr
 
 
+def pin_band_edge_rule(mod=DG):
+    """A bin exactly on an edge belongs to the band above it (edges[k] <= nu <
+    edges[k+1]), and nu = 1 to the last band.  On a 1x8 tile nu = 2 kx / 8
+    exactly, so a cosine at kx = 2 (nu = 1/2) with edges (0, 1/2, 1) puts all
+    of its energy in band 1, and one at kx = 4 (nu = 1) too."""
+    x = np.arange(8)[None, :]
+    for kx in (2, 4):
+        f = np.cos(2 * math.pi * kx * x / 8)[:, :, None]
+        fr = mod.band_energy(f, np.zeros_like(f), 1, 8, [0.0, 0.5, 1.0], eps=0.0)
+        assert np.allclose(fr, [0.0, 1.0], rtol=0, atol=1e-12), (kx, fr)
+
+
 def _bandlimit(x):
     """Zero the Nyquist row and column, so fractional translations are exact."""
     X = np.fft.rfft2(x, axes=(0, 1))
@@ -171,7 +183,8 @@ def pin_frame_diagnostics_translation(mod=DG):
 
 PINS = [pin_nrmse, pin_band_parseval, pin_band_single_frequency, pin_band_split,
         pin_phase_error_translation,
-        pin_phase_progress, pin_oracle_corrections, pin_frame_diagnostics_translation]
+        pin_phase_progress, pin_oracle_corrections, pin_frame_diagnostics_translation,
+        pin_band_edge_rule]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])

@@ -180,6 +180,7 @@ SOURCE_MUTANTS = {
     "route_budget_off_by_one": (R, "route", "k_eff = min(int(topk), M)",
                                 "k_eff = int(topk) if int(topk) <= M else M - 1"),
     "coupled_pooled_scores_unscaled": (OC, "pooled_stats", "s = scale * (qb @ kb.T)", "s = (qb @ kb.T)"),
+    "band_edge_goes_low": (DG, "band_index", 'side="right"', 'side="left"'),
 }
 
 
@@ -193,7 +194,7 @@ def test_source_mutation_caught(name):
     ns = dict(mod.__dict__)
     exec(compile(bad, "<mutant>", "exec"), ns)
     mm = clone(mod, **{fn: ns[fn]})
-    pins = {P: TP.PINS, R: TR.ROUTE_PINS, OC: TC.PINS}[mod]
+    pins = {P: TP.PINS, R: TR.ROUTE_PINS, OC: TC.PINS, DG: TDG.PINS}[mod]
     assert _any_pin_fails(mm, pins), f"no pin catches mutation {name}"
 
 
