@@ -134,6 +134,35 @@ def test_route_many_chunks(cast_lib, M):
     for topk in (1, 7, 64, 100):
         check_route(cast_lib, q, k, topk, 0.125, f"M{M} k{topk}")
 
+def test_route_workspace_reuse(cast_lib):
+    """One workspace serves consecutive calls of different shapes (channel groups
+    of one, two or four heads, a partial last group; rank-count and bitonic
+    selection): each call must match a call on a fresh workspace bit for bit, so
+    nothing a call leaves in the workspace reaches the next one."""
+    dev = "cuda"
+    shapes = [  # n_a, S, H, dh, M, Bv, topk
+        (3, 100, 12, 128, 16, 70, 4),
+        (2, 33, 5, 64, 40, 17, 7),
+        (4, 50, 3, 32, 9, 31, 2),
+        (1, 64, 6, 32, 256, 8, 30),
+        (2, 40, 3, 64, 300, 12, 9),
+        (3, 100, 12, 128, 16, 70, 4),
+    ]
+    nb = max(cast_lib.cast_route_kv_workspace_bytes(*s[:6]) for s in shapes)
+    ws = torch.full((nb,), 0x7f, dtype=torch.uint8, device=dev)
+    for j, (n_a, S, H, dh, M, Bv, topk) in enumerate(shapes):
+        torch.manual_seed(900 + j)
+        q = torch.randn(n_a, S, H, dh, device=dev).to(torch.bfloat16)
+        k = (torch.randn(M, Bv, H, dh, device=dev)
+             + torch.randn(M, 1, H, dh, device=dev)).to(torch.bfloat16)
+        for _ in range(2):
+            a = cast_lib.cast_route_kv(q, k, topk, 0.2, want_scores=True, workspace=ws)
+            b = cast_lib.cast_route_kv(q, k, topk, 0.2, want_scores=True)
+            torch.cuda.synchronize()
+            assert torch.equal(a[0], b[0]) and torch.equal(a[2], b[2]), (j, n_a, H, dh, M)
+        check_route(cast_lib, q, k, topk, 0.2, f"reuse{j}")
+
+
 def test_route_deterministic(cast_lib):
     w = gen.get(W.MATRIX)
     q, k, _, _, _ = gen.attn_inputs(w, seed=3, device="cuda")
@@ -414,6 +443,49 @@ def check_par(cast_lib, resid_np, anchors, *, accumulate=False, gate_mode=0, x0=
         dth = np.minimum(dth, 2 * np.pi - dth)
         assert dth.max() <= 1e-3, dth.max()
     return out
+
+
+def test_par_workspace_reuse_and_long_target_runs(cast_lib):
+    """One workspace serves consecutive PAR calls of different shapes (the fused
+    8x8 launches with edge classes, a 4x4 tiling launched per class, several pairs,
+    long runs of targets between and beyond the anchors, a pair with no interior
+    frame).  Each call matches a call on a fresh workspace bit for bit and the
+    oracle within the PAR bar."""
+    dev = "cuda"
+    rng = np.random.default_rng(77)
+    cases = [  # n_frames, Hg, Wg, D, anchors, tile, accumulate
+        (45, 13, 19, 64, (2, 40), 8, False),
+        (9, 16, 16, 96, (0, 3, 8), 4, True),
+        (40, 9, 10, 40, (5, 6, 30), 8, True),
+        (45, 13, 19, 64, (2, 40), 8, False),
+    ]
+    nb = 0
+    for (n, hg, wg, d, anc, tile, acc) in cases:
+        prm = cast_lib.cast_par_params_default(tile_h=tile, tile_w=tile)
+        nb = max(nb, cast_lib.cast_par_workspace_bytes(n, len(anc), hg, wg, d, prm))
+    ws = torch.full((nb,), 0x7f, dtype=torch.uint8, device=dev)
+    for j, (n, hg, wg, d, anc, tile, acc) in enumerate(cases):
+        base = rng.standard_normal((hg, wg, d))
+        resid_np = np.zeros((n, hg, wg, d))
+        for m, f in enumerate(anc):
+            resid_np[f] = np.roll(base, (m, 2 * m), axis=(0, 1)) + 0.2 * rng.standard_normal(base.shape)
+        x0 = rng.standard_normal(resid_np.shape)
+        resid = torch.from_numpy(resid_np.astype(np.float32)).to(dev)
+        prm = cast_lib.cast_par_params_default(accumulate=int(acc), tile_h=tile, tile_w=tile)
+        outs = []
+        for use_ws in (True, False):
+            out = torch.from_numpy(x0.astype(np.float32)).to(dev)
+            cast_lib.cast_par_reconstruct(resid, anc, prm, out=out, workspace=ws if use_ws else None)
+            torch.cuda.synchronize()
+            outs.append(out)
+        assert torch.equal(outs[0], outs[1]), j
+        oprm = OP.ParParams(tile_h=tile, tile_w=tile, accumulate=acc)
+        ref = OP.par_reconstruct(resid_np.astype(np.float32).astype(np.float64), anc, oprm,
+                                 out=x0.astype(np.float32).astype(np.float64))
+        sk = [t for t in range(n) if t not in set(anc)]
+        rr = rel_rms(outs[0].cpu().numpy().astype(np.float64)[sk], ref[sk])
+        log(f"[par reuse {j}] rel-RMS {rr:.3e} over {len(sk)} frames")
+        assert rr <= PAR_REL_RMS, (j, rr)
 
 
 def test_par_tiny_all_modes(cast_lib):
