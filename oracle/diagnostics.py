@@ -16,7 +16,8 @@ orthonormal real 2-D DFT, real-FFT multiplicities kappa, normalised radius nu):
   alpha theta_p)| averaged with energy weights kappa |F_t|^2 (bins where F_t or
   F_a vanishes carry no phase and no weight);
 * phase progress of one coefficient: (phi_t - phi_a) / (phi_b - phi_a) on phases
-  unwrapped along the frames.
+  unwrapped along the frames; phase_progress_frames takes it for every stored bin
+  of every tile and channel over the interior frames of each anchor pair.
 
 Readings where the paper leaves a choice: the bands are given by edges on PAR's nu
 (band k holds edges[k] <= nu < edges[k+1], the last band also nu = 1); the energy
@@ -119,6 +120,29 @@ def phase_progress(phases, ia: int, ib: int) -> np.ndarray:
     """eq:phase_progress for every frame of one coefficient's phase track."""
     u = unwrap_track(phases)
     return (u - u[ia]) / (u[ib] - u[ia])
+
+
+def phase_progress_frames(ref, anchors, tile_h: int, tile_w: int) -> np.ndarray:
+    """eq:phase_progress for every coefficient: tile p, stored bin (ky, kx) of its
+    real 2-D DFT, channel c, and every interior frame t of each adjacent anchor
+    pair (a, b).  The track of one coefficient is Arg F_t for t = a .. b (the
+    orthonormal tile transform of App. A.2, edge tiles at their own size),
+    unwrapped along the frames and normalised by its displacement between the two
+    anchors.  Returns p [n_frames, n_tiles, tile_h, tile_w // 2 + 1, D]: NaN on
+    anchor frames, frames outside [a_0, a_last] and slots past an edge tile's bins
+    (and where the displacement vanishes, 0 / 0)."""
+    ref = np.asarray(ref, dtype=np.float64)
+    n, Hg, Wg, D = ref.shape
+    tl = P.tiles(Hg, Wg, tile_h, tile_w)
+    out = np.full((n, len(tl), tile_h, tile_w // 2 + 1, D), np.nan)
+    for (a, b) in P.anchor_pairs(anchors):
+        for p, (y0, hp, x0, wp) in enumerate(tl):
+            ph = np.stack([np.angle(P.rfft2_ortho(ref[t, y0:y0 + hp, x0:x0 + wp]))
+                           for t in range(a, b + 1)])
+            with np.errstate(divide="ignore", invalid="ignore"):
+                prog = phase_progress(ph, 0, b - a)
+            out[a + 1:b, p, :hp, :wp // 2 + 1, :] = prog[1:-1]
+    return out
 
 
 def frame_diagnostics(ref, approx, anchors, prm: P.ParParams, edges, eps: float = EPS):

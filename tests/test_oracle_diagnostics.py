@@ -140,6 +140,42 @@ def pin_phase_progress(mod=DG):
     assert np.allclose(p, (frames - 1) / 4.0, rtol=0, atol=1e-12)
 
 
+def pin_phase_progress_frames(mod=DG):
+    """Every 4x4 tile of an 8x12 grid moves circularly by its own integer step per
+    frame, so each coefficient turns by the same angle every frame (eq:shift): where
+    that angle is not +-pi and the coefficient is nonzero the progress of an
+    interior frame t of the pair (a, b) is (t - a)/(b - a), per pair (anchors 0, 3
+    and 7), and every other entry is NaN."""
+    r = rng(11)
+    n, th, tw, D = 9, 4, 4, 3
+    steps = [(1, 0), (0, 1), (1, 1), (3, 1), (2, 3), (1, 2)]
+    ref = np.zeros((n, 8, 12, D))
+    tl = P.tiles(8, 12, th, tw)
+    for p, (y0, hp, x0, wp) in enumerate(tl):
+        base = r.standard_normal((hp, wp, D))
+        for t in range(n):
+            ref[t, y0:y0 + hp, x0:x0 + wp] = np.roll(base, (t * steps[p][0], t * steps[p][1]), axis=(0, 1))
+    anchors = (0, 3, 7)
+    got = mod.phase_progress_frames(ref, anchors, th, tw)
+    assert got.shape == (n, len(tl), th, tw // 2 + 1, D)
+    ky = np.arange(th)[:, None]
+    kx = np.arange(tw // 2 + 1)[None, :]
+    checked = 0
+    for p, (y0, hp, x0, wp) in enumerate(tl):
+        turn = 2 * math.pi * (ky * steps[p][0] / hp + kx * steps[p][1] / wp)
+        ok = np.abs(np.abs(DG.wrap_pm_pi(turn)) - math.pi) > 1e-6
+        F0 = P.rfft2_ortho(ref[0, y0:y0 + hp, x0:x0 + wp])
+        for (a, b) in [(0, 3), (3, 7)]:
+            for t in range(a + 1, b):
+                sel = ok[:, :, None] & (np.abs(F0) > 1e-9) & (np.abs(DG.wrap_pm_pi(turn)) > 1e-9)[:, :, None]
+                g = got[t, p]
+                assert np.allclose(g[sel], (t - a) / (b - a), rtol=0, atol=1e-9), (p, t)
+                checked += int(sel.sum())
+    assert checked > 100
+    for t in (0, 3, 7, 8):
+        assert np.isnan(got[t]).all(), t
+
+
 def pin_oracle_corrections(mod=DG):
     """eq:oracles: when the reference is the linear interpolation both
     corrections return it; when the reference has the magnitudes of the linear
@@ -183,7 +219,8 @@ def pin_frame_diagnostics_translation(mod=DG):
 
 PINS = [pin_nrmse, pin_band_parseval, pin_band_single_frequency, pin_band_split,
         pin_phase_error_translation,
-        pin_phase_progress, pin_oracle_corrections, pin_frame_diagnostics_translation,
+        pin_phase_progress, pin_phase_progress_frames, pin_oracle_corrections,
+        pin_frame_diagnostics_translation,
         pin_band_edge_rule]
 
 

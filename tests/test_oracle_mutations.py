@@ -181,6 +181,11 @@ SOURCE_MUTANTS = {
                                 "k_eff = int(topk) if int(topk) <= M else M - 1"),
     "coupled_pooled_scores_unscaled": (OC, "pooled_stats", "s = scale * (qb @ kb.T)", "s = (qb @ kb.T)"),
     "band_edge_goes_low": (DG, "band_index", 'side="right"', 'side="left"'),
+    "progress_frames_shifted": (DG, "phase_progress_frames", "= prog[1:-1]", "= prog[:-2]"),
+    "progress_frames_wrong_end": (DG, "phase_progress_frames", "phase_progress(ph, 0, b - a)",
+                                  "phase_progress(ph, 0, b - a - 1)"),
+    "progress_frames_not_unwrapped": (DG, "phase_progress_frames", "prog = phase_progress(ph, 0, b - a)",
+                                      "prog = (ph - ph[0]) / (ph[-1] - ph[0])"),
 }
 
 
