@@ -386,7 +386,7 @@ def main():
 
     # spectral diagnostics of the skipped frames (validation, not inference): error
     # ratio, band energies, transport phase error and both oracle corrections
-    diag_ms = None
+    diag_ms = prog_ms = None
     if w.has_par and not args.step_only:
         s1, _ = cast.par_debug_shapes(w.n_a, w.Hg, w.Wg, prm)
         theta = torch.zeros(s1, device=dev)
@@ -407,6 +407,21 @@ def main():
         dm[1].record(stream)
         torch.cuda.synchronize()
         diag_ms = dm[0].elapsed_time(dm[1]) / n_diag
+        del dws
+        # phase progress of every coefficient over each pair's interior frames
+        dprm = cast.cast_diag_params_default()
+        n_tiles = -(-w.Hg // dprm.tile_h) * -(-w.Wg // dprm.tile_w)
+        pp = torch.empty((w.n_frames, n_tiles, dprm.tile_h * (dprm.tile_w // 2 + 1), w.D),
+                         dtype=torch.float32, device=dev)
+        cast.cast_phase_progress(s0["resid"], w.anchors, dprm, p_out=pp, stream=stream)
+        torch.cuda.synchronize()
+        dm[0].record(stream)
+        for _ in range(n_diag):
+            cast.cast_phase_progress(s0["resid"], w.anchors, dprm, p_out=pp, stream=stream)
+        dm[1].record(stream)
+        torch.cuda.synchronize()
+        prog_ms = dm[0].elapsed_time(dm[1]) / n_diag
+        del pp
 
     value = w.frame_tokens / (ms_step / 1e3)
     res = {
@@ -423,7 +438,8 @@ def main():
                    "attn_input_seeds": seeds if w.has_attention else None},
         "per_call_ms": {"route": route_ms, "attn": attn_ms, "par": par_ms,
                         "route_coupled": coupled_ms, "par_block_update": block_ms,
-                        "frame_select": sel_ms, "spectral_diagnostics": diag_ms},
+                        "frame_select": sel_ms, "spectral_diagnostics": diag_ms,
+                        "phase_progress": prog_ms},
         "per_call_ms_median": {c: float(np.median(v)) for c, v in per_call.items()
                                if isinstance(v, list)},
     }

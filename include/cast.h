@@ -435,6 +435,32 @@ cast_status_t cast_spectral_diagnostics(const float* ref, const float* approx, c
                                         float* r_phase_out, float* r_mag_out, void* workspace,
                                         size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * Phase progress of every coefficient (App. C eq:phase_progress), for the interior
+ * frames of each adjacent anchor pair (a, b): with F_t the orthonormal real 2-D
+ * DFT of tile p and channel c of ref[t] (params->tile_h x tile_w tiles, edge tiles
+ * at their own size) and, for each stored bin (ky, kx), the phase unwrapped along
+ * the frames,
+ *   u_a = 0,  u_t = u_{t-1} + wrap_[-pi,pi)(Arg F_t - Arg F_{t-1})  (t = a+1 .. b),
+ *   p_out[t, p, ky * (tile_w/2 + 1) + kx, c] = u_t / u_b          (a < t < b).
+ * Uniform progression gives alpha = (t - a)/(b - a) (eq:shift).  Entries of
+ * anchor frames, of frames before the first or after the last anchor, and of slots
+ * past a smaller edge tile's bins are not written; a vanishing displacement u_b
+ * gives +-inf or NaN (IEEE division).
+ *
+ * ref      fp32 [n_frames, Hg, Wg, D] device: residuals of every frame.
+ * anchors  HOST int[n_anchor], strictly increasing in [0, n_frames), n_anchor >= 2.
+ * params   the tiling (tile_h, tile_w); the band fields must be valid but are unused.
+ * p_out    fp32 [n_frames, n_tiles, tile_h * (tile_w/2 + 1), D] device,
+ *          n_tiles = ceil(Hg/tile_h) * ceil(Wg/tile_w), row-major.
+ * Errors: CAST_ERR_NULL (ref, anchors, params, p_out), CAST_ERR_SHAPE (sizes,
+ * misaligned buffers), CAST_ERR_ANCHORS, CAST_ERR_UNSUPPORTED (tile edges above 8,
+ * n_frames > 4096, n_anchor > 512).  Reference-based: for validation, not inference.
+ */
+cast_status_t cast_phase_progress(const float* ref, const int* anchors, int n_anchor, int n_frames,
+                                  int Hg, int Wg, int D, const cast_diag_params_t* params,
+                                  float* p_out, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

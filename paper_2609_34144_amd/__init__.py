@@ -29,7 +29,8 @@ EXPORTED = ["cast_status_string", "cast_last_error_detail", "cast_abi_version",
             "cast_coupled_params_default", "cast_wo_gram", "cast_route_coupled_workspace_bytes",
             "cast_route_coupled", "cast_select_params_default",
             "cast_frame_select_workspace_bytes", "cast_frame_select", "cast_diag_params_default",
-            "cast_spectral_diagnostics_workspace_bytes", "cast_spectral_diagnostics"]
+            "cast_spectral_diagnostics_workspace_bytes", "cast_spectral_diagnostics",
+            "cast_phase_progress"]
 
 
 class CastError(RuntimeError):
@@ -132,6 +133,9 @@ def load(path: str = LIB_PATH):
     lib.cast_spectral_diagnostics.argtypes = [_vp, _vp, _vp, _c.POINTER(_i), _i, _i, _i, _i, _i,
                                               _c.POINTER(DiagParams), _vp, _vp, _vp, _vp, _vp,
                                               _vp, _sz, _vp]
+    lib.cast_phase_progress.restype = _i
+    lib.cast_phase_progress.argtypes = [_vp, _c.POINTER(_i), _i, _i, _i, _i, _i,
+                                        _c.POINTER(DiagParams), _vp, _vp]
     _lib = lib
     return lib
 
@@ -343,6 +347,27 @@ def cast_spectral_diagnostics(ref, approx, anchors, params: DiagParams | None = 
                                          _ptr(bands), _ptr(perr), _ptr(rp), _ptr(rm), _ptr(ws), wsb,
                                          _stream(stream)))
     return {"nrmse": nrmse, "bands": bands, "phase_err": perr, "r_phase": rp, "r_mag": rm}
+
+
+def cast_phase_progress(ref, anchors, params: DiagParams | None = None, p_out=None, stream=None):
+    """Phase progress of every coefficient over the interior frames of each anchor
+    pair.  ref fp32 [n_frames, Hg, Wg, D] (device).  Returns p fp32 [n_frames,
+    n_tiles, tile_h * (tile_w // 2 + 1), D]; entries the call does not write keep
+    p_out's values (NaN when p_out is None)."""
+    import torch
+    lib = load()
+    if params is None:
+        params = cast_diag_params_default()
+    n_frames, Hg, Wg, D = ref.shape
+    nt = -(-Hg // params.tile_h) * -(-Wg // params.tile_w)
+    if p_out is None:
+        p_out = torch.full((n_frames, nt, params.tile_h * (params.tile_w // 2 + 1), D), float("nan"),
+                           dtype=torch.float32, device=ref.device)
+    anc = [int(a) for a in anchors]
+    arr = (ctypes.c_int * max(len(anc), 1))(*anc)
+    _check(lib.cast_phase_progress(_ptr(ref), arr, len(anc), n_frames, Hg, Wg, D,
+                                   ctypes.byref(params), _ptr(p_out), _stream(stream)))
+    return p_out
 
 
 def cast_anchor_attn_workspace_bytes(n_a, S, H, dh, k_eff, n0, Bv) -> int:

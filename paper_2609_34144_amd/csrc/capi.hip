@@ -505,4 +505,24 @@ cast_status_t cast_spectral_diagnostics(const float* ref, const float* approx, c
                      nrmse_out, band_out, phase_err_out, r_phase_out, r_mag_out, workspace, stream);
 }
 
+cast_status_t cast_phase_progress(const float* ref, const int* anchors, int n_anchor, int n_frames,
+                                  int Hg, int Wg, int D, const cast_diag_params_t* params,
+                                  float* p_out, hipStream_t stream) {
+  if (ref == nullptr || anchors == nullptr || p_out == nullptr)
+    return fail(CAST_ERR_NULL, "progress: ref, anchors and p_out are required");
+  cast_status_t st = diag_check(n_frames, Hg, Wg, D, params);
+  if (st != CAST_OK) return st;
+  if (n_anchor < 2 || n_anchor > n_frames || n_anchor > kParMaxAnchors)
+    return fail(CAST_ERR_ANCHORS, "progress: need 2 <= n_anchor <= min(n_frames, %d)", kParMaxAnchors);
+  for (int j = 0; j < n_anchor; ++j) {
+    if (anchors[j] < 0 || anchors[j] >= n_frames)
+      return fail(CAST_ERR_ANCHORS, "progress: anchor %d = %d outside [0, %d)", j, anchors[j], n_frames);
+    if (j > 0 && anchors[j] <= anchors[j - 1])
+      return fail(CAST_ERR_ANCHORS, "progress: anchors must be strictly increasing (index %d)", j);
+  }
+  if (!aligned(ref, 4) || !aligned(p_out, 4)) return fail(CAST_ERR_SHAPE, "progress: misaligned buffers");
+  return launch_phase_progress(ref, anchors, n_anchor, Hg, Wg, D, params->tile_h, params->tile_w,
+                               p_out, stream);
+}
+
 }  // extern "C"

@@ -141,5 +141,8 @@ cast_status_t launch_diag(const float* ref, const float* approx, const float* th
                           const cast_diag_params_t& p, float* nrmse_out, float* band_out,
                           float* phase_err_out, float* r_phase_out, float* r_mag_out, void* ws,
                           hipStream_t stream);
+cast_status_t launch_phase_progress(const float* ref, const int* anchors, int n_anchor, int Hg,
+                                    int Wg, int D, int tile_h, int tile_w, float* p_out,
+                                    hipStream_t stream);
 
 }  // namespace cast

@@ -6,6 +6,8 @@
 //             writing one partial per (frame, tile, channel block of 256).
 // diag_final  one wave per frame: the partials in fixed order (fp64), then e_t,
 //             the band fractions and the phase error.
+// diag_progress<HP, WP>  (diag_device.h) the phase progress of every coefficient,
+//             one launch per tile shape.
 #include "diag_device.h"
 
 namespace cast {
@@ -131,6 +133,42 @@ cast_status_t launch_diag(const float* ref, const float* approx, const float* th
   f.n_anchor = n_anchor;
   hipLaunchKernelGGL(diag_final_kernel, dim3(n_frames), dim3(64), 0, stream, f);
   return check_launch("diag_final");
+}
+
+cast_status_t launch_phase_progress(const float* ref, const int* anchors, int n_anchor, int Hg,
+                                    int Wg, int D, int tile_h, int tile_w, float* p_out,
+                                    hipStream_t stream) {
+  diagdev::ProgArgs a{};
+  a.ref = ref;
+  a.p_out = p_out;
+  a.frame_elems = (long long)Hg * Wg * D;
+  a.Hg = Hg;
+  a.Wg = Wg;
+  a.D = D;
+  a.tile_h = tile_h;
+  a.tile_w = tile_w;
+  a.n_tx = (Wg + tile_w - 1) / tile_w;
+  a.n_tiles = a.n_tx * ((Hg + tile_h - 1) / tile_h);
+  for (int j = 0; j < n_anchor; ++j) a.anchors[j] = (short)anchors[j];
+  const int n_chblk = (D + kDiagThreads - 1) / kDiagThreads;
+  const int nfy = Hg / tile_h, hr = Hg % tile_h, nfx = Wg / tile_w, wr = Wg % tile_w;
+  struct Cls { int ty0, tx0, nty, ntx, hp, wp; } cls[4];
+  int ncls = 0;
+  if (nfy > 0 && nfx > 0) cls[ncls++] = {0, 0, nfy, nfx, tile_h, tile_w};
+  if (nfy > 0 && wr > 0) cls[ncls++] = {0, nfx, nfy, 1, tile_h, wr};
+  if (hr > 0 && nfx > 0) cls[ncls++] = {nfy, 0, 1, nfx, hr, tile_w};
+  if (hr > 0 && wr > 0) cls[ncls++] = {nfy, nfx, 1, 1, hr, wr};
+  for (int k = 0; k < ncls; ++k) {
+    a.ty0 = cls[k].ty0;
+    a.tx0 = cls[k].tx0;
+    a.ntx_c = cls[k].ntx;
+    hipLaunchKernelGGL(diag_row(cls[k].hp).p[cls[k].wp - 1],
+                       dim3(cls[k].nty * cls[k].ntx, n_chblk, n_anchor - 1), dim3(kDiagThreads), 0,
+                       stream, a);
+    cast_status_t st = check_launch("diag_progress");
+    if (st != CAST_OK) return st;
+  }
+  return CAST_OK;
 }
 
 }  // namespace cast

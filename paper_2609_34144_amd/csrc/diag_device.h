@@ -46,6 +46,17 @@ struct DiagArgs {
 
 typedef void (*DiagTileFn)(DiagArgs);
 
+struct ProgArgs {
+  const float* ref;
+  float* p_out;            // [n_frames, n_tiles, tile_h * (tile_w / 2 + 1), D]
+  long long frame_elems;
+  int Hg, Wg, D, tile_h, tile_w, n_tx, n_tiles;
+  int ty0, tx0, ntx_c;     // the tile class of this launch, as in DiagArgs
+  short anchors[kParMaxAnchors];
+};
+
+typedef void (*DiagProgFn)(ProgArgs);
+
 // Frame-wide buffer resource (a frame is below 4 GB); an element is addressed as
 // (lane channel + tile row, in a VGPR) + (column within the tile, uniform, SGPR).
 constexpr int kBufDword3 = 0x00020000;   // 32-bit data format, gfx9-family V#
@@ -61,6 +72,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t frame_rsrc(const float* base, 
 // compiled in its own translation unit).
 struct DiagRow {
   DiagTileFn k[8];
+  DiagProgFn p[8];
 };
 void diag_row_1(DiagRow& r);
 void diag_row_2(DiagRow& r);
@@ -293,6 +305,81 @@ __global__ __launch_bounds__(kDiagThreads) void diag_tile(DiagArgs a) {
     float s = 0.0f;
     for (int w = 0; w < kDiagThreads / 64; ++w) s += s_red[w][tid];
     a.partial[(((long long)t * a.n_tiles + tile) * a.n_chblk + chb) * kVals + tid] = s;
+  }
+}
+
+// Phase progress (App. C eq:phase_progress) of one tile shape: grid (tile of the
+// class, channel block of 256, anchor pair (a, b)).  Each thread owns one channel
+// of one tile and walks the frames a..b twice.  Frame by frame it transforms the
+// tile, takes the phase Arg F_t of every stored bin and unwraps it along the
+// frames, u_t = u_{t-1} + wrap_[-pi,pi)(Arg F_t - Arg F_{t-1}) with u_a = 0; the
+// first walk ends with the displacement u_b, the second stores u_t / u_b for the
+// interior frames.  Anchor frames, frames outside the pairs and slots past a
+// smaller tile's bins are not written.
+template <int HP, int WP>
+__global__ __launch_bounds__(kDiagThreads) void diag_progress(ProgArgs a) {
+  constexpr int NKX = WP / 2 + 1;
+  const int i_cls = blockIdx.x, chb = blockIdx.y, pr = blockIdx.z;
+  const int fa = a.anchors[pr], fb = a.anchors[pr + 1];
+  const int ty = a.ty0 + i_cls / a.ntx_c, tx = a.tx0 + (i_cls - (i_cls / a.ntx_c) * a.ntx_c);
+  const int tile = ty * a.n_tx + tx;
+  const int y0 = ty * a.tile_h, x0 = tx * a.tile_w;
+  const int c_raw = chb * kDiagThreads + (int)threadIdx.x;
+  const bool live = c_raw < a.D;
+  const int c = live ? c_raw : a.D - 1;
+  const unsigned lane_off = (unsigned)c * 4u + (unsigned)(((long long)y0 * a.Wg + x0) * a.D * 4);
+  const unsigned row_bytes = (unsigned)((long long)a.Wg * a.D * 4), col_bytes = (unsigned)a.D * 4u;
+  const float* const ref = a.ref;
+  const long long frame_elems = a.frame_elems;
+  auto phases = [&](int t, float (&ph)[HP][NKX]) {
+    const __amdgpu_buffer_rsrc_t r = frame_rsrc(ref, t, frame_elems);
+    float Fr[HP][NKX], Fi[HP][NKX];
+    fwd_tile<HP, WP>([&](int y, float (&v)[WP]) {
+      const unsigned vo = lane_off + (unsigned)y * row_bytes;
+#pragma unroll
+      for (int x = 0; x < WP; ++x)
+        v[x] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)vo, (int)(x * col_bytes), 0));
+    }, Fr, Fi);
+#pragma unroll
+    for (int ky = 0; ky < HP; ++ky)
+#pragma unroll
+      for (int kx = 0; kx < NKX; ++kx) ph[ky][kx] = atan2f(Fi[ky][kx], Fr[ky][kx]);
+  };
+  auto wrap = [](float x) { return x - 2.0f * kPi * floorf((x + kPi) * (0.5f / kPi)); };
+  float prev[HP][NKX], u[HP][NKX], den[HP][NKX];
+  for (int pass = 0; pass < 2; ++pass) {
+    phases(fa, prev);
+#pragma unroll
+    for (int ky = 0; ky < HP; ++ky)
+#pragma unroll
+      for (int kx = 0; kx < NKX; ++kx) u[ky][kx] = 0.0f;
+    const int t_end = pass == 0 ? fb : fb - 1;
+    for (int t = fa + 1; t <= t_end; ++t) {
+      float ph[HP][NKX];
+      phases(t, ph);
+#pragma unroll
+      for (int ky = 0; ky < HP; ++ky)
+#pragma unroll
+        for (int kx = 0; kx < NKX; ++kx) {
+          u[ky][kx] += wrap(ph[ky][kx] - prev[ky][kx]);
+          prev[ky][kx] = ph[ky][kx];
+        }
+      if (pass == 1 && live) {
+        const int nkx_out = a.tile_w / 2 + 1;
+        float* dst = a.p_out + ((long long)t * a.n_tiles + tile) * (long long)(a.tile_h * nkx_out) * a.D + c;
+#pragma unroll
+        for (int ky = 0; ky < HP; ++ky)
+#pragma unroll
+          for (int kx = 0; kx < NKX; ++kx)
+            __builtin_nontemporal_store(u[ky][kx] / den[ky][kx], dst + (long long)(ky * nkx_out + kx) * a.D);
+      }
+    }
+    if (pass == 0) {
+#pragma unroll
+      for (int ky = 0; ky < HP; ++ky)
+#pragma unroll
+        for (int kx = 0; kx < NKX; ++kx) den[ky][kx] = u[ky][kx];
+    }
   }
 }
 

@@ -1,5 +1,5 @@
-// Spectral-diagnostics tile kernels of one tile height: this file is compiled
-// once per height CAST_DIAG_HP in 1..8, for widths 1..8.
+// Spectral-diagnostics and phase-progress tile kernels of one tile height: this
+// file is compiled once per height CAST_DIAG_HP in 1..8, for widths 1..8.
 #include "diag_device.h"
 
 #ifndef CAST_DIAG_HP
@@ -22,6 +22,14 @@ void CAST_CAT(diag_row_, CAST_DIAG_HP)(DiagRow& r) {
   r.k[5] = diag_tile<HP, 6>;
   r.k[6] = diag_tile<HP, 7>;
   r.k[7] = diag_tile<HP, 8>;
+  r.p[0] = diag_progress<HP, 1>;
+  r.p[1] = diag_progress<HP, 2>;
+  r.p[2] = diag_progress<HP, 3>;
+  r.p[3] = diag_progress<HP, 4>;
+  r.p[4] = diag_progress<HP, 5>;
+  r.p[5] = diag_progress<HP, 6>;
+  r.p[6] = diag_progress<HP, 7>;
+  r.p[7] = diag_progress<HP, 8>;
 }
 
 }  // namespace diagdev

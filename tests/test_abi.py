@@ -331,6 +331,29 @@ def test_diag_validation(lib):
     assert nb > 0 and nb % 256 == 0
 
 
+def _prog(lib, *, ref=A, anchors=(0, 3), n_frames=4, Hg=8, Wg=8, D=64, p_out=2 * A, params=None, **pkw):
+    p = params if params is not None else cast.cast_diag_params_default(**pkw)
+    arr = (ctypes.c_int * max(len(anchors), 1))(*anchors)
+    return lib.cast_phase_progress(ref, arr, len(anchors), n_frames, Hg, Wg, D, ctypes.byref(p),
+                                   p_out, None)
+
+
+def test_phase_progress_validation(lib):
+    assert _prog(lib, ref=None) == NULL
+    assert _prog(lib, p_out=None) == NULL
+    assert lib.cast_phase_progress(A, None, 2, 4, 8, 8, 64, ctypes.byref(cast.cast_diag_params_default()),
+                                   2 * A, None) == NULL
+    assert lib.cast_phase_progress(A, (ctypes.c_int * 2)(0, 3), 2, 4, 8, 8, 64, None, 2 * A, None) == NULL
+    assert _prog(lib, anchors=(1,)) == ANCHORS
+    assert _prog(lib, anchors=(3, 1)) == ANCHORS
+    assert _prog(lib, anchors=(0, 4)) == ANCHORS
+    assert _prog(lib, tile_w=9) == UNSUPPORTED
+    assert _prog(lib, n_frames=5000, anchors=(0, 3)) == UNSUPPORTED
+    assert _prog(lib, D=0) == SHAPE
+    assert _prog(lib, p_out=2 * A + 2) == SHAPE
+    assert _prog(lib, ref=A + 1) == SHAPE
+
+
 def test_binding_wraps_every_entry_point():
     """The Python binding carries every C entry point under its own name."""
     missing = [n for n in cast.EXPORTED

@@ -1,5 +1,6 @@
-"""GPU parity of the spectral diagnostics (cast_spectral_diagnostics) against the
-oracle (oracle/diagnostics.py) on identical inputs: generator ground-truth
+"""GPU parity of the spectral diagnostics (cast_spectral_diagnostics, and
+cast_phase_progress at the end) against the oracle (oracle/diagnostics.py) on
+identical inputs: generator ground-truth
 residuals of every frame as the reference, the GPU PAR reconstruction (write mode)
 as the approximation, and each side's own PAR transport phases.
 
@@ -180,3 +181,101 @@ def test_diag_tile_shapes(cast_lib):
         ref = np.stack([np.roll(base, (t, -t), axis=(0, 1)) + 0.3 * rng.standard_normal((Hg, Wg, D))
                         for t in range(5)])
         run_case(cast_lib, ref, (0, 2, 4), f"{Hg}x{Wg}x{D} tile {tile}", tile=tile)
+
+
+# ---- phase progress (eq:phase_progress)
+# A track (one coefficient over the frames a..b of a pair) is compared where float64
+# puts it clear of the decisions fp32 cannot follow: |F_t| >= PROG_MAG times its
+# tile column's norm at every frame, every wrapped step at least PROG_STEP from
+# +-pi, and a displacement |u_b| >= PROG_DEN.  There the bar is the propagated fp32
+# error: an 8x8 orthonormal DFT in fp32 is within 16 eps ||column|| of exact per bin,
+# so Arg F_s is within e_s = 16 eps ||column_s|| / |F_s| + 3e-7 (atan2), u_t within
+# E_t = 2 (e_a + ... + e_t), and p_t = u_t / u_b within (E_t + |p_t| E_b) / |u_b|.
+PROG_MAG, PROG_STEP, PROG_DEN = 1e-3, 1e-2, 5e-2
+EPS32 = 2.0 ** -24
+
+
+def progress_case(cast_lib, ref_np, anchors, tile, label):
+    dev = "cuda"
+    th, tw = (tile, tile) if np.isscalar(tile) else tile
+    ref = torch.from_numpy(ref_np.astype(np.float32)).to(dev)
+    dprm = cast_lib.cast_diag_params_default(tile_h=th, tile_w=tw)
+    got = cast_lib.cast_phase_progress(ref, anchors, dprm)
+    torch.cuda.synchronize()
+    ref64 = ref.cpu().numpy().astype(np.float64)
+    want = DG.phase_progress_frames(ref64, anchors, th, tw)          # [n, tiles, th, nkx, D]
+    n, Hg, Wg, D = ref64.shape
+    nkx = tw // 2 + 1
+    g = got.cpu().numpy().astype(np.float64).reshape(n, -1, th, nkx, D)
+    tl = OP.tiles(Hg, Wg, th, tw)
+    defined = np.zeros(g.shape, dtype=bool)
+    well = np.zeros(g.shape, dtype=bool)
+    bound = np.zeros(g.shape)
+    for (a, b) in OP.anchor_pairs(anchors):
+        for p, (y0, hp, x0, wp) in enumerate(tl):
+            defined[a + 1:b, p, :hp, :wp // 2 + 1, :] = True
+            F = np.stack([OP.rfft2_ortho(ref64[t, y0:y0 + hp, x0:x0 + wp]) for t in range(a, b + 1)])
+            norm = np.sqrt((np.abs(F) ** 2).sum(axis=(1, 2)))[:, None, None, :]
+            steps = DG.wrap_pm_pi(np.diff(np.angle(F), axis=0))
+            ok = ((np.abs(F) >= PROG_MAG * norm).all(axis=0)
+                  & (np.abs(np.abs(steps) - np.pi) > PROG_STEP).all(axis=0)
+                  & (np.abs(steps.sum(axis=0)) >= PROG_DEN))
+            with np.errstate(divide="ignore"):
+                e = 16 * EPS32 * norm / np.abs(F) + 3e-7
+            E = 2.0 * np.cumsum(e, axis=0)                            # E_t for t = a .. b
+            ub = np.abs(steps.sum(axis=0))
+            pw = np.abs(want[a + 1:b, p, :hp, :wp // 2 + 1, :])
+            well[a + 1:b, p, :hp, :wp // 2 + 1, :] = ok[None]
+            bound[a + 1:b, p, :hp, :wp // 2 + 1, :] = (E[1:-1] + pw * E[-1][None]) / ub[None]
+    # the entries the call must leave alone keep the NaN fill
+    assert np.isnan(g[~defined]).all(), label
+    err = np.abs(g[well] - want[well])
+    frac = well.sum() / max(defined.sum(), 1)
+    log(f"[progress {label}] max |dp| {err.max():.2e}, max |dp| / bound "
+        f"{(err / bound[well]).max():.2f}, over {int(well.sum())} entries ({frac:.1%} of the defined ones)")
+    assert frac > 0.5, (label, frac)
+    assert (err <= bound[well] + 1e-6).all(), (label, (err / bound[well]).max())
+    return g, want, well
+
+
+def test_phase_progress_translation(cast_lib):
+    """Per-tile circular translations by a fixed integer step per frame: every
+    coefficient turns by the same angle each frame, so the progress is alpha."""
+    rng = np.random.default_rng(31)
+    n, th, tw, D = 9, 8, 8, 70
+    Hg, Wg = 16, 24
+    steps = [(1, 0), (0, 1), (1, 1), (3, 1), (2, 3), (1, 2)]
+    ref = np.zeros((n, Hg, Wg, D))
+    for p, (y0, hp, x0, wp) in enumerate(OP.tiles(Hg, Wg, th, tw)):
+        base = rng.standard_normal((hp, wp, D))
+        for t in range(n):
+            ref[t, y0:y0 + hp, x0:x0 + wp] = np.roll(base, (t * steps[p][0], t * steps[p][1]), axis=(0, 1))
+    g, want, well = progress_case(cast_lib, ref, (0, 3, 7), 8, "translation")
+    for (a, b) in ((0, 3), (3, 7)):
+        for t in range(a + 1, b):
+            # (turns of exactly +-pi are outside `well`: fp32 may wrap them either way)
+            sel = well[t] & (np.abs(want[t] - (t - a) / (b - a)) < 1e-9)
+            assert sel.sum() > 1000
+            assert np.abs(g[t][sel] - (t - a) / (b - a)).max() <= 1e-4, (t,)
+
+
+@pytest.mark.parametrize("tile", [8, 4, (5, 3)])
+def test_phase_progress_moving_field_and_edge_tiles(cast_lib, tile):
+    """A 1/f^2 field moved by a sub-token step per frame plus noise, on a grid whose
+    edges leave smaller tiles; three anchors (two pairs, one with four interior
+    frames), frames before the first and after the last anchor, channels past a
+    multiple of 256."""
+    rng = np.random.default_rng(5)
+    from gen.workloads import fourier_shift, power_law_field
+    base = power_law_field(13, 19, 300, 2.0, rng)
+    d = np.array([0.35, -0.6])
+    ref = np.stack([fourier_shift(base, d * t) + 0.05 * rng.standard_normal(base.shape)
+                    for t in range(10)])
+    progress_case(cast_lib, ref, (1, 4, 9), tile, f"tile {tile}")
+
+
+def test_phase_progress_matrix_like(cast_lib):
+    """The Matrix-Game-like block with the generator's ground-truth skipped frames."""
+    w = gen.get(W.MATRIX)
+    ref, _, _ = gen.par_inputs(w, seed=42, frames="all", D=256)
+    progress_case(cast_lib, ref, w.anchors, 8, "matrix-like")
