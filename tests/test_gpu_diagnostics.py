@@ -195,7 +195,7 @@ PROG_MAG, PROG_STEP, PROG_DEN = 1e-3, 1e-2, 5e-2
 EPS32 = 2.0 ** -24
 
 
-def progress_case(cast_lib, ref_np, anchors, tile, label):
+def progress_case(cast_lib, ref_np, anchors, tile, label, min_frac=0.5):
     dev = "cuda"
     th, tw = (tile, tile) if np.isscalar(tile) else tile
     ref = torch.from_numpy(ref_np.astype(np.float32)).to(dev)
@@ -233,7 +233,7 @@ def progress_case(cast_lib, ref_np, anchors, tile, label):
     frac = well.sum() / max(defined.sum(), 1)
     log(f"[progress {label}] max |dp| {err.max():.2e}, max |dp| / bound "
         f"{(err / bound[well]).max():.2f}, over {int(well.sum())} entries ({frac:.1%} of the defined ones)")
-    assert frac > 0.5, (label, frac)
+    assert frac > min_frac, (label, frac)
     assert (err <= bound[well] + 1e-6).all(), (label, (err / bound[well]).max())
     return g, want, well
 
@@ -279,3 +279,17 @@ def test_phase_progress_matrix_like(cast_lib):
     w = gen.get(W.MATRIX)
     ref, _, _ = gen.par_inputs(w, seed=42, frames="all", D=256)
     progress_case(cast_lib, ref, w.anchors, 8, "matrix-like")
+
+
+def test_phase_progress_tile_shapes(cast_lib):
+    """Tile shapes with edges 1, 2, 3 and 7 (each shape has its own kernel), a pair
+    with no interior frame (anchors 2, 3), and channels past a multiple of 256:
+    15x9 with 8x8 tiles gives 8x8, 8x1, 7x8 and 7x1; 5x7 with 2x3 tiles gives 2x3,
+    2x1, 1x3 and 1x1 (whose real bins carry phases 0 or pi only, most of them
+    outside the compared tracks)."""
+    rng = np.random.default_rng(14)
+    for (Hg, Wg, D, tile, min_frac) in [(15, 9, 40, 8, 0.5), (5, 7, 300, (2, 3), 0.2)]:
+        base = rng.standard_normal((Hg, Wg, D))
+        ref = np.stack([np.roll(base, (t, -t), axis=(0, 1)) + 0.3 * rng.standard_normal((Hg, Wg, D))
+                        for t in range(7)])
+        progress_case(cast_lib, ref, (0, 2, 3, 6), tile, f"{Hg}x{Wg}x{D} tile {tile}", min_frac)
