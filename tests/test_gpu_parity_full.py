@@ -61,14 +61,15 @@ def route_and_check(cast_lib, q, k, topk, scale, s_or, label):
     return idx, k_eff
 
 
-def attn_sampled(cast_lib, w, q, k, v, idx, k_eff, pairs, n_rows, label, seed=0):
+def attn_sampled(cast_lib, w, q, k, v, idx, k_eff, pairs, n_rows, label, seed=0, extra_rows=()):
     out, lse = cast_lib.cast_anchor_attn(q, k, v, idx, k_eff, w.scale, want_lse=True)
     torch.cuda.synchronize()
     rng = np.random.default_rng(seed)
     idx_np = idx.cpu().numpy()
     got_all, ref_all = [], []
     for (i, h) in pairs:
-        rows = sorted(set(int(s) for s in rng.choice(w.S, n_rows, replace=False)) | {0, w.S - 1})
+        rows = sorted(set(int(s) for s in rng.choice(w.S, n_rows, replace=False)) | {0, w.S - 1}
+                      | set(extra_rows))
         # host copies of just this pair's routed chunks (head h), then the oracle's gather
         sel = torch.as_tensor(idx_np[i, h], dtype=torch.long, device=k.device)
         k_sub = np64(k.index_select(0, sel)[:, :, h:h + 1, :])
@@ -94,10 +95,26 @@ def test_route_attn_hy_like(cast_lib):
     attn_sampled(cast_lib, w, q, k, v, idx, k_eff, pairs, 24, "hy sampled")
 
 
+def test_attn_hy_like_every_pair(cast_lib):
+    """Every (anchor, head) pair of the HY-like block (96 pairs), among them the
+    pairs whose work units form the last, partial round and run as key pieces
+    merged afterwards (the last 64 of 1344 units), a few rows each: the first and
+    last query, rows at the borders of the last 256-query tile (24 queries past
+    the last full tile), and random rows."""
+    w = gen.get(W.HY)
+    q, k, v, _, _ = gen.attn_inputs(w, seed=42, device="cuda")
+    idx, k_eff, _ = cast_lib.cast_route_kv(q, k, w.topk, w.scale)
+    last = (w.S - 1) // 256 * 256
+    pairs = [(i, h) for i in range(w.n_a) for h in range(w.H)]
+    attn_sampled(cast_lib, w, q, k, v, idx, k_eff, pairs, 3, "hy every pair", seed=1,
+                 extra_rows=(last, last + 31, last - 256, last - 1))
+
+
 def test_route_attn_long_history(cast_lib):
     """All four budgets of the long-history workload share one input; the routing
     decisions are checked for every (anchor, head) at each budget, and attention
-    on sampled rows of three (anchor, head) pairs at every budget."""
+    on sampled rows of three (anchor, head) pairs at every budget, of every pair at
+    the budget of 8 and of twelve pairs at 32."""
     w = gen.get("long_history_4f44x80_d3072_k32")
     q, k, v, _, _ = gen.attn_inputs(w, seed=42, device="cuda")
     s_or = oracle_scores_chunked(q, k, w.scale)
@@ -105,6 +122,14 @@ def test_route_attn_long_history(cast_lib):
         idx, k_eff = route_and_check(cast_lib, q, k, topk, w.scale, s_or, f"long k{topk}")
         attn_sampled(cast_lib, w, q, k, v, idx, k_eff, [(0, 3), (2, 17), (3, 23)], 16,
                      f"long k{topk} sampled")
+        if topk == 8:
+            attn_sampled(cast_lib, w, q, k, v, idx, k_eff,
+                         [(i, h) for i in range(w.n_a) for h in range(w.H)], 2,
+                         "long k8 every pair", seed=2)
+        if topk == 32:
+            attn_sampled(cast_lib, w, q, k, v, idx, k_eff,
+                         [(i, 2 * j + i % 2) for i in range(w.n_a) for j in range(0, 12, 4)], 4,
+                         "long k32 twelve pairs", seed=3)
 
 
 def par_sampled(cast_lib, w, targets, accumulate, label, debug=False):
