@@ -99,8 +99,8 @@ def test_attn_hy_like_every_pair(cast_lib):
     """Every (anchor, head) pair of the HY-like block (96 pairs), among them the
     pairs whose work units form the last, partial round and run as key pieces
     merged afterwards (the last 64 of 1344 units), a few rows each: the first and
-    last query, rows at the borders of the last 256-query tile (24 queries past
-    the last full tile), and random rows."""
+    last query, rows at the borders of the last query tile (192 of 256 queries),
+    and random rows."""
     w = gen.get(W.HY)
     q, k, v, _, _ = gen.attn_inputs(w, seed=42, device="cuda")
     idx, k_eff, _ = cast_lib.cast_route_kv(q, k, w.topk, w.scale)
