@@ -19,6 +19,7 @@ import time
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libcast.so")
+CLIENT = os.path.join(HERE, "cast_client")
 BUILD = os.path.join(os.path.dirname(HERE), "_build")
 
 ARCH = "gfx950"
@@ -88,8 +89,16 @@ def build(verbose: bool = True, jobs: int = 0) -> str:
         print("[build]", " ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, OUT)
+    # a C-ABI client with no Python (tests/test_gpu_c_client.py runs it)
+    ctmp = CLIENT + ".tmp"
+    cmd = [cc, "-O2", "-std=c++17", f"--offload-arch={ARCH}", os.path.join(CSRC, "cast_client.cpp"),
+           "-o", ctmp, "-L" + HERE, "-lcast", "-Wl,-rpath,$ORIGIN"]
     if verbose:
-        print(f"[build] {OUT} ({time.time() - t0:.1f} s)", flush=True)
+        print("[build]", " ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(ctmp, CLIENT)
+    if verbose:
+        print(f"[build] {OUT} and {CLIENT} ({time.time() - t0:.1f} s)", flush=True)
     return OUT
 
 
