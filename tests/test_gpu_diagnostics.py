@@ -220,13 +220,14 @@ def progress_case(cast_lib, ref_np, anchors, tile, label, min_frac=0.5):
             ok = ((np.abs(F) >= PROG_MAG * norm).all(axis=0)
                   & (np.abs(np.abs(steps) - np.pi) > PROG_STEP).all(axis=0)
                   & (np.abs(steps.sum(axis=0)) >= PROG_DEN))
-            with np.errstate(divide="ignore"):
+            # (only the well-conditioned entries use the bound; the others may divide by 0)
+            with np.errstate(divide="ignore", invalid="ignore"):
                 e = 16 * EPS32 * norm / np.abs(F) + 3e-7
-            E = 2.0 * np.cumsum(e, axis=0)                            # E_t for t = a .. b
-            ub = np.abs(steps.sum(axis=0))
-            pw = np.abs(want[a + 1:b, p, :hp, :wp // 2 + 1, :])
+                E = 2.0 * np.cumsum(e, axis=0)                        # E_t for t = a .. b
+                ub = np.abs(steps.sum(axis=0))
+                pw = np.abs(want[a + 1:b, p, :hp, :wp // 2 + 1, :])
+                bound[a + 1:b, p, :hp, :wp // 2 + 1, :] = (E[1:-1] + pw * E[-1][None]) / ub[None]
             well[a + 1:b, p, :hp, :wp // 2 + 1, :] = ok[None]
-            bound[a + 1:b, p, :hp, :wp // 2 + 1, :] = (E[1:-1] + pw * E[-1][None]) / ub[None]
     # the entries the call must leave alone keep the NaN fill
     assert np.isnan(g[~defined]).all(), label
     err = np.abs(g[well] - want[well])
