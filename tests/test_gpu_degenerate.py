@@ -3,7 +3,9 @@ closed forms they reduce to: one query and one key (attention returns that key's
 value row), one history chunk of one token, fewer chunks than the budget; PAR on
 one-token frames and single channels (a 1x1 tile's DFT is the identity and its one
 bin is self-conjugate, so PAR is the linear interpolation / extrapolation of
-eq:block), and a pair of adjacent anchors with nothing to reconstruct."""
+eq:block), and a pair of adjacent anchors with nothing to reconstruct.  Then the
+largest sizes the boundary accepts: 4096 chunks, 1024 routed chunks, 4096 frames
+with 512 anchors."""
 import math
 
 import numpy as np
@@ -110,3 +112,58 @@ def test_par_single_channel_and_adjacent_anchors(cast_lib):
     cast_lib.cast_par_reconstruct(two, (0, 1), cast_lib.cast_par_params_default(), out=out2)
     torch.cuda.synchronize()
     assert (out2 == 5.0).all()
+
+
+# ---- the largest sizes the boundary accepts
+def test_route_4096_chunks(cast_lib):
+    """M = 4096 chunks (the bitonic selection's whole LDS key array) with exact ties."""
+    from test_gpu_parity import check_route
+    dev = "cuda"
+    torch.manual_seed(4096)
+    q = torch.randn(2, 3, 2, 32, device=dev).to(torch.bfloat16)
+    k = torch.randn(4096, 2, 2, 32, device=dev).to(torch.bfloat16)
+    k[4095] = k[17]
+    print("[max sizes] route M 4096", flush=True)
+    for topk in (1, 1000, 4096):
+        check_route(cast_lib, q, k, topk, 0.2, f"M4096 k{topk}")
+
+
+def test_attn_1024_routed_chunks(cast_lib):
+    """k_eff = 1024 routed chunks (the most the kernel takes) of 3 tokens each, with
+    a current segment: 3,104 keys, the general copy mode, the key split."""
+    from test_gpu_parity import check_attn
+    dev = "cuda"
+    torch.manual_seed(1024)
+    n_a, S, H, dh, M, Bv, n0 = 1, 40, 1, 64, 1500, 3, 32
+    q = torch.randn(n_a, S, H, dh, device=dev).to(torch.bfloat16)
+    k = torch.randn(M, Bv, H, dh, device=dev).to(torch.bfloat16)
+    v = torch.randn(M, Bv, H, dh, device=dev).to(torch.bfloat16)
+    kc = torch.randn(n0, H, dh, device=dev).to(torch.bfloat16)
+    vc = torch.randn(n0, H, dh, device=dev).to(torch.bfloat16)
+    rng = np.random.default_rng(1024)
+    idx = torch.tensor(np.sort(rng.choice(M, size=(n_a, H, 1024), replace=True), axis=-1),
+                       dtype=torch.int32, device=dev)
+    print("[max sizes] attention k_eff 1024", flush=True)
+    check_attn(cast_lib, q, k, v, idx, 1024, 1 / math.sqrt(dh), kc=kc, vc=vc, label="k_eff 1024")
+
+
+def test_par_4096_frames_512_anchors(cast_lib):
+    """n_frames = 4096 and n_anchor = 512 (the largest accepted), 511 pairs with
+    frames before the first anchor and after the last, write and accumulate modes."""
+    dev = "cuda"
+    rng = np.random.default_rng(512)
+    n = 4096
+    anchors = tuple(range(3, n, 8))[:512]
+    resid = np.zeros((n, 2, 3, 2))
+    for a in anchors:
+        resid[a] = rng.standard_normal((2, 3, 2))
+    print(f"[max sizes] PAR {n} frames, {len(anchors)} anchors", flush=True)
+    ref = OP.par_reconstruct(resid.astype(np.float32).astype(np.float64), anchors, OP.ParParams())
+    out = torch.zeros(resid.shape, device=dev)
+    cast_lib.cast_par_reconstruct(torch.from_numpy(resid.astype(np.float32)).to(dev), anchors,
+                                  cast_lib.cast_par_params_default(), out=out)
+    torch.cuda.synchronize()
+    sk = [t for t in range(n) if t not in set(anchors)]
+    got = out.cpu().numpy().astype(np.float64)
+    assert rel_rms(got[sk], ref[sk]) <= PAR_REL_RMS
+    assert (got[list(anchors)] == 0.0).all()
