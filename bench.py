@@ -292,6 +292,21 @@ def main():
         torch.cuda.synchronize()
         return a.elapsed_time(b) / args.steps
 
+    # the spread: every step (and below, every call) once more, each between its
+    # own pair of events; the headline stays the bracketed loop above
+    def each_timed(fn, n):
+        evs = [(ev(), ev()) for _ in range(n)]
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(evs):
+            a.record(stream)
+            fn(i)
+            b.record(stream)
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) for (a, b) in evs]
+
+    step_each = each_timed(lambda i: (graphs[i % N_COPIES].replay() if graphs
+                                      else step(sets[i % N_COPIES])), args.steps)
+
     per_call = {}
     route_ms = attn_ms = 0.0
     if w.has_attention:
@@ -310,6 +325,19 @@ def main():
     par_ms = timed_loop(lambda s: cast.cast_par_reconstruct(
         s["resid"], w.anchors, prm, out=s["x"], workspace=par_ws, stream=stream)) if w.has_par else 0.0
     per_call.update(route=route_ms, attn=attn_ms, par=par_ms)
+    call_median = {}
+    if w.has_attention:
+        call_median["route"] = float(np.median(each_timed(lambda i: cast.cast_route_kv(
+            sets[i % N_COPIES]["q"], sets[i % N_COPIES]["k"], w.topk, w.scale, idx_out=idx,
+            workspace=route_ws, stream=stream), args.steps)))
+        call_median["attn"] = float(np.median(each_timed(lambda i: cast.cast_anchor_attn(
+            sets[i % N_COPIES]["q"], sets[i % N_COPIES]["k"], sets[i % N_COPIES]["v"],
+            sets[i % N_COPIES]["idx"], k_eff, w.scale, out=attn_out, workspace=attn_ws,
+            stream=stream), args.steps)))
+    if w.has_par:
+        call_median["par"] = float(np.median(each_timed(lambda i: cast.cast_par_reconstruct(
+            sets[i % N_COPIES]["resid"], w.anchors, prm, out=sets[i % N_COPIES]["x"],
+            workspace=par_ws, stream=stream), args.steps)))
 
     # reconstruction-coupled routing (NEXT-1), timed on its own after the step;
     # the W_O Gram matrices depend on weights only and are prepared once, untimed
@@ -440,8 +468,11 @@ def main():
                         "route_coupled": coupled_ms, "par_block_update": block_ms,
                         "frame_select": sel_ms, "spectral_diagnostics": diag_ms,
                         "phase_progress": prog_ms},
-        "per_call_ms_median": {c: float(np.median(v)) for c, v in per_call.items()
-                               if isinstance(v, list)},
+        "per_call_ms_median": {**call_median,
+                               **{c: float(np.median(v)) for c, v in per_call.items()
+                                  if isinstance(v, list)}},
+        "ms_per_step_each": {"median": float(np.median(step_each)), "min": float(min(step_each)),
+                             "max": float(max(step_each))},
     }
     extra = {}
     traffic = load_traffic(w.name)
