@@ -28,6 +28,8 @@
 // launches are 1-D grids that give each XCD a contiguous part of each pair's
 // (tile, channel block) range (fused_block_work), so the waves of one XCD sweep
 // neighbouring tiles of the same frames.
+#include <algorithm>
+
 #include "par_device.h"
 
 namespace cast {
@@ -332,14 +334,21 @@ cast_status_t launch_par(const float* resid, const int* anchors, int n_anchor, i
   a.accumulate = p.accumulate;
   a.update_anchors = p.update_anchors;
   for (int j = 0; j < n_anchor; ++j) a.anchors[j] = (short)anchors[j];
-  // gate grid: (tile, pair, chunk of kGateTargets targets of the pair)
+  // gate grid: (tile, pair, chunk of kGateTargets targets of the pair); the frames
+  // each pair's reconstruction blocks write (targets, and anchors when updated)
+  // order the fused reconstruction launch, most first (ties by pair index)
   int max_targets = 0;
+  int work[kParMaxAnchors];
   for (int pr = 0; pr + 1 < n_anchor; ++pr) {
     int n = anchors[pr + 1] - anchors[pr] - 1;
     if (pr == 0) n += anchors[0];
     if (pr + 2 == n_anchor) n += n_frames - anchors[n_anchor - 1] - 1;
     max_targets = n > max_targets ? n : max_targets;
+    work[pr] = n + (p.update_anchors ? (pr + 2 == n_anchor ? 2 : 1) : 0);
+    a.recon_order[pr] = (short)pr;
   }
+  std::stable_sort(a.recon_order, a.recon_order + (n_anchor - 1),
+                   [&](short x, short y) { return work[x] > work[y]; });
   const dim3 gate_grid(pl.n_tiles, pl.n_pairs,
                        max_targets > 0 ? (max_targets + kGateTargets - 1) / kGateTargets : 1);
 

@@ -27,6 +27,10 @@ struct ParArgs {
   float tau_low, tau_high, q, T, eta_rel, eta_abs, eps;
   int gate_mode, accumulate, update_anchors;
   short anchors[kParMaxAnchors];
+  // the fused reconstruction launch takes the pairs in this order: most targets
+  // first, so the blocks that walk the longest target lists start first and the
+  // launch ends on short ones
+  short recon_order[kParMaxAnchors];
 };
 
 struct TileGeom {
@@ -465,6 +469,7 @@ __global__ __launch_bounds__(64) void par_recon_fused(ParArgs a, ClassSet cs,
   __shared__ float fb_lds[2 * kBins * kChb];
   int tile_b, chb, pair;
   fused_block_work(blockIdx.x, cs.end[3], a.n_chblk, tile_b, chb, pair);
+  pair = a.recon_order[pair];
   for_class<HR, WR>(a, cs, tile_b, [&](auto hp, auto wp, int tile) {
     recon_block<decltype(hp)::value, decltype(wp)::value, ACC, NTT>(a, tile, chb, pair, resid, out,
                                                                    coef, fb_lds);
