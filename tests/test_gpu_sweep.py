@@ -11,6 +11,7 @@ anchors with and without frames before the first / after the last anchor
 (eq:block extrapolation), write and accumulate modes and the three gate modes.
 """
 import math
+import os
 
 import numpy as np
 import pytest
@@ -20,8 +21,10 @@ from test_gpu_parity import check_attn, check_par, check_route
 
 pytestmark = pytest.mark.gpu
 
-ATTN_CASES = list(range(24))
-PAR_CASES = list(range(24))
+# CAST_SWEEP_CASES widens the sweep (default 24 cases of each kind)
+_N = int(os.environ.get("CAST_SWEEP_CASES", "24"))
+ATTN_CASES = list(range(_N))
+PAR_CASES = list(range(_N))
 
 
 def attn_case(seed):
