@@ -46,27 +46,9 @@ __global__ __launch_bounds__(64) void par_xspec_kernel(ParArgs a, TileClass k,
   xspec_block<HP, WP>(a, class_tile(a, k, blockIdx.x), blockIdx.y, blockIdx.z, resid, partial, lds);
 }
 
-// ---------------------------------------------------------------------------
-// par_gate
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ float wave_sum(float v) {
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-__device__ __forceinline__ float wave_max(float v) {
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
-}
-
-// Principal argument in (-pi, pi].
-__device__ __forceinline__ float wrap_arg(float y, float x) {
-  float t = atan2f(y, x);
-  const float kPiF = 3.14159265358979323846f;
-  return (t == -kPiF) ? kPiF : t;
-}
-
 constexpr int kGateTargets = 8;   // targets per gate block
 constexpr int kGateWaves = 4;     // waves per gate block
+constexpr int kInlineBlocksPerCU = 7;   // resident reconstruction blocks with the gate inline
 
 __global__ __launch_bounds__(64 * kGateWaves) void par_gate_kernel(ParArgs a,
                                                                     const float* __restrict__ partial,
@@ -76,23 +58,14 @@ __global__ __launch_bounds__(64 * kGateWaves) void par_gate_kernel(ParArgs a,
   const int tile = blockIdx.x, pair = blockIdx.y;
   const TileGeom g = tile_geom(a, tile);
   const int wv = threadIdx.x >> 6, b = threadIdx.x & 63;
-  const int ky = b / kNkx, kx = b - (b / kNkx) * kNkx;
   const int H = g.hp, W = g.wp;
-  const bool active = b < kBins && ky < H && kx <= W / 2;
-  const bool hc = kx == 0 || (W % 2 == 0 && 2 * kx == W);
-  int kind = 0;  // 0 representative, 1 mirror, 2 self-conjugate
-  int sky = ky;  // row of the slot whose partial sums hold this bin's values
-  if (hc) {
-    int mky = (H - ky) % H;
-    if (mky == ky) kind = 2;
-    else if (2 * ky > H) { kind = 1; sky = mky; }
-  }
+  const BinSlot bs = bin_slot(b, H, W);
   // wave wv sums its quarter of the channel blocks' partials, in block order
   {
     float zr = 0.0f, zi = 0.0f, w = 0.0f;
-    if (active) {
+    if (bs.active) {
       const float* src = partial + ((long long)pair * a.n_tiles + tile) * a.n_chblk * kVals +
-                         (sky * kNkx + kx) * 3;
+                         (bs.sky * kNkx + bs.kx) * 3;
       const int j0 = a.n_chblk * wv / kGateWaves, j1 = a.n_chblk * (wv + 1) / kGateWaves;
 #pragma unroll 4
       for (int j = j0; j < j1; ++j) {
@@ -108,55 +81,25 @@ __global__ __launch_bounds__(64 * kGateWaves) void par_gate_kernel(ParArgs a,
   __syncthreads();
   if (wv == 0) {
     float zr = 0.0f, zi = 0.0f, w = 0.0f;
-    if (active) {
+    if (bs.active) {
 #pragma unroll
       for (int q = 0; q < kGateWaves; ++q) {
         zr += part[q][0][b];
         zi += part[q][1][b];
         w += part[q][2][b];
       }
-      const float nrm = 1.0f / (float)(H * W);   // orthonormal scaling of both spectra
-      zr *= nrm;
-      zi *= nrm;
-      w *= nrm;
-      if (kind == 1) zi = -zi;                    // mirror = conjugate of its representative
     }
-    const float wmax = wave_max(active ? w : 0.0f);
-    const float eta = a.eta_rel * wmax + a.eta_abs;
-    const float zabs = sqrtf(zr * zr + zi * zi);
-    const bool rel = active && (w > eta) && (zabs > eta);
-    float theta = 0.0f;
-    if (rel && kind == 0) theta = wrap_arg(zi, zr);
-    if (rel && kind == 1) theta = -wrap_arg(-zi, zr);
-    const bool omega_plus = rel && !(ky == 0 && kx == 0);
-    const float kappa = hc ? 1.0f : 2.0f;
-    const float num = wave_sum(omega_plus ? kappa * zabs : 0.0f);
-    const float den = wave_sum(omega_plus ? kappa * w : 0.0f);
-    const int n_plus = __popcll(__ballot(omega_plus));
-    const float conf = n_plus > 0 ? num / (den + a.eps) : 0.0f;
-    // nu: physical radius of the bin over the largest stored radius of the tile
-    const int kys = (2 * ky <= H) ? ky : ky - H;
-    const float fy = (float)kys / (float)H, fx = (float)kx / (float)W;
-    const float my = (float)(H / 2) / (float)H, mx = (float)(W / 2) / (float)W;
-    const float rmax = sqrtf(my * my + mx * mx);
-    const float nu = rmax > 0.0f ? sqrtf(fy * fy + fx * fx) / rmax : 0.0f;
-    float gate;
-    if (a.gate_mode == 1) gate = 1.0f;
-    else if (a.gate_mode == 2) gate = 0.0f;
-    else {
-      const float tau = a.tau_low + (a.tau_high - a.tau_low) * powf(nu, a.q);
-      gate = 1.0f / (1.0f + expf(-(conf - tau) / a.T));
-    }
+    const BinGate bg = bin_gate(a, bs, H, W, zr, zi, w);
     // optional diagnostics, laid out per the caller's tile_h x (tile_w/2+1) rows
     // (written by the first target chunk)
     const int nkx_out = a.tile_w / 2 + 1;
-    if (blockIdx.z == 0 && b < kBins && ky < a.tile_h && kx < nkx_out) {
-      const long long o = ((long long)pair * a.n_tiles + tile) * a.bins_out + ky * nkx_out + kx;
-      if (a.theta_out) a.theta_out[o] = active ? theta : 0.0f;
-      if (a.gate_out) a.gate_out[o] = active ? gate : 0.0f;
+    if (blockIdx.z == 0 && b < kBins && bs.ky < a.tile_h && bs.kx < nkx_out) {
+      const long long o = ((long long)pair * a.n_tiles + tile) * a.bins_out + bs.ky * nkx_out + bs.kx;
+      if (a.theta_out) a.theta_out[o] = bs.active ? bg.theta : 0.0f;
+      if (a.gate_out) a.gate_out[o] = bs.active ? bg.gate : 0.0f;
     }
-    if (a.conf_out && b == 0 && blockIdx.z == 0) a.conf_out[(long long)pair * a.n_tiles + tile] = conf;
-    tg[b] = make_float2(theta, gate);
+    if (a.conf_out && b == 0 && blockIdx.z == 0) a.conf_out[(long long)pair * a.n_tiles + tile] = bg.conf;
+    tg[b] = make_float2(bg.theta, bg.gate);
   }
   __syncthreads();
   if (b >= kBins) return;
@@ -169,20 +112,10 @@ __global__ __launch_bounds__(64 * kGateWaves) void par_gate_kernel(ParArgs a,
   const int n_in = fb - fa - 1, n_lo = pair == 0 ? fa : 0;
   const int n_hi = pair == n_pairs - 1 ? a.n_frames - fb - 1 : 0;
   const int k0 = blockIdx.z * kGateTargets, k1 = min(k0 + kGateTargets, n_in + n_lo + n_hi);
-  const float inv_gap = 1.0f / (float)(fb - fa);
-  const float nrm = 1.0f / (float)(H * W);
   for (int k = k0 + wv; k < k1; k += kGateWaves) {
     const int t = k < n_in ? fa + 1 + k : (k < n_in + n_lo ? k - n_in : fb + 1 + (k - n_in - n_lo));
-    const float alpha = (float)(t - fa) * inv_gap;
-    float4 cf = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    if (active) {
-      float sa, ca, sb, cb;
-      sincosf(gate * alpha * theta, &sa, &ca);
-      sincosf(-gate * (1.0f - alpha) * theta, &sb, &cb);
-      const float wa = (1.0f - alpha) * nrm, wb = alpha * nrm;
-      cf = make_float4(wa * ca, wa * sa, wb * cb, wb * sb);
-    }
-    coef[((long long)t * a.n_tiles + tile) * kBins + b] = cf;
+    coef[((long long)t * a.n_tiles + tile) * kBins + b] = blend_coef(t, fa, fb, theta, gate, H, W,
+                                                                      bs.active);
   }
 }
 
@@ -371,14 +304,25 @@ cast_status_t launch_par(const float* resid, const int* anchors, int n_anchor, i
     hipLaunchKernelGGL(row.xspec[wi], grid, dim3(kChb), 0, stream, a, cs, resid, partial);
     st = check_launch("par_xspec");
     if (st != CAST_OK) return st;
-    hipLaunchKernelGGL(par_gate_kernel, gate_grid, dim3(64 * kGateWaves), 0, stream, a,
-                       (const float*)partial, coef);
-    st = check_launch("par_gate");
-    if (st != CAST_OK) return st;
+    // When the reconstruction grid fits in one round of resident blocks (kInlineBlocksPerCU
+    // per compute unit: the register file allows 8, LDS with the coefficients 7), each
+    // block computes its tile's gate itself, and the gate launch, a serial step of
+    // its own, goes; the debug outputs come from the gate launch.
+    const int cus = device_cu_count();
+    const bool inl = theta_out == nullptr && gate_out == nullptr && conf_out == nullptr && cus > 0 &&
+                     (long long)grid.x <= (long long)kInlineBlocksPerCU * cus;
+    if (!inl) {
+      hipLaunchKernelGGL(par_gate_kernel, gate_grid, dim3(64 * kGateWaves), 0, stream, a,
+                         (const float*)partial, coef);
+      st = check_launch("par_gate");
+      if (st != CAST_OK) return st;
+    }
     // accumulate mode with several pairs: stream the targets (see recon_body)
-    const ReconFusedFn rf = !p.accumulate ? row.recon_w[wi]
-                            : (pl.n_pairs > 1 ? row.recon_as[wi] : row.recon_a[wi]);
-    hipLaunchKernelGGL(rf, grid, dim3(kChb), 0, stream, a, cs, resid, out, (const float4*)coef);
+    const ReconFusedFn rf = !p.accumulate ? (inl ? row.inl_w[wi] : row.recon_w[wi])
+                            : (pl.n_pairs > 1 ? (inl ? row.inl_as[wi] : row.recon_as[wi])
+                                              : (inl ? row.inl_a[wi] : row.recon_a[wi]));
+    hipLaunchKernelGGL(rf, grid, dim3(kChb), 0, stream, a, cs, resid, out, (const float4*)coef,
+                       (const float*)partial);
     return check_launch("par_recon");
   }
   // other tilings: one launch per tile class and pass

@@ -215,6 +215,111 @@ __device__ __forceinline__ void xspec_block(const ParArgs& a, int tile, int chb,
 }
 
 // ---------------------------------------------------------------------------
+// The gate of one stored bin (App. A.2, eq:confidence, eq:gate), one lane per bin
+// slot b of a wave: from the channel sums (Z, W) of the bin's slot, eta over the
+// tile's stored bins, reliability, theta (representative / mirror /
+// self-conjugate), c_p over the tile, nu and g.  Every lane of the wave takes part
+// (wave reductions); lanes outside the tile's bins pass active = false.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float wave_sum(float v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+// Principal argument in (-pi, pi].
+__device__ __forceinline__ float wrap_arg(float y, float x) {
+  float t = atan2f(y, x);
+  const float kPiF = 3.14159265358979323846f;
+  return (t == -kPiF) ? kPiF : t;
+}
+
+// Which slot holds bin b's sums: Hermitian columns store their rows ky <= H/2;
+// a mirror row reads its representative's slot and conjugates it.
+struct BinSlot {
+  int ky, kx, sky, kind;   // kind 0 representative, 1 mirror, 2 self-conjugate
+  bool active, hc;
+};
+__device__ __forceinline__ BinSlot bin_slot(int b, int H, int W) {
+  BinSlot r;
+  r.ky = b / kNkx;
+  r.kx = b - r.ky * kNkx;
+  r.active = b < kBins && r.ky < H && r.kx <= W / 2;
+  r.hc = r.kx == 0 || (W % 2 == 0 && 2 * r.kx == W);
+  r.kind = 0;
+  r.sky = r.ky;
+  if (r.hc) {
+    const int mky = (H - r.ky) % H;
+    if (mky == r.ky) r.kind = 2;
+    else if (2 * r.ky > H) { r.kind = 1; r.sky = mky; }
+  }
+  return r;
+}
+
+struct BinGate {
+  float theta, gate, conf;
+};
+// zr, zi, w: the slot's sums over all channels of F_b conj(F_a) and |F_b||F_a|
+// (unnormalised transforms).
+__device__ __forceinline__ BinGate bin_gate(const ParArgs& a, const BinSlot& s, int H, int W,
+                                            float zr, float zi, float w) {
+  if (s.active) {
+    const float nrm = 1.0f / (float)(H * W);   // orthonormal scaling of both spectra
+    zr *= nrm;
+    zi *= nrm;
+    w *= nrm;
+    if (s.kind == 1) zi = -zi;                  // mirror = conjugate of its representative
+  } else {
+    zr = zi = w = 0.0f;
+  }
+  const float wmax = wave_max(s.active ? w : 0.0f);
+  const float eta = a.eta_rel * wmax + a.eta_abs;
+  const float zabs = sqrtf(zr * zr + zi * zi);
+  const bool rel = s.active && (w > eta) && (zabs > eta);
+  BinGate r;
+  r.theta = 0.0f;
+  if (rel && s.kind == 0) r.theta = wrap_arg(zi, zr);
+  if (rel && s.kind == 1) r.theta = -wrap_arg(-zi, zr);
+  const bool omega_plus = rel && !(s.ky == 0 && s.kx == 0);
+  const float kappa = s.hc ? 1.0f : 2.0f;
+  const float num = wave_sum(omega_plus ? kappa * zabs : 0.0f);
+  const float den = wave_sum(omega_plus ? kappa * w : 0.0f);
+  const int n_plus = __popcll(__ballot(omega_plus));
+  r.conf = n_plus > 0 ? num / (den + a.eps) : 0.0f;
+  // nu: physical radius of the bin over the largest stored radius of the tile
+  const int kys = (2 * s.ky <= H) ? s.ky : s.ky - H;
+  const float fy = (float)kys / (float)H, fx = (float)s.kx / (float)W;
+  const float my = (float)(H / 2) / (float)H, mx = (float)(W / 2) / (float)W;
+  const float rmax = sqrtf(my * my + mx * mx);
+  const float nu = rmax > 0.0f ? sqrtf(fy * fy + fx * fx) / rmax : 0.0f;
+  if (a.gate_mode == 1) r.gate = 1.0f;
+  else if (a.gate_mode == 2) r.gate = 0.0f;
+  else {
+    const float tau = a.tau_low + (a.tau_high - a.tau_low) * powf(nu, a.q);
+    r.gate = 1.0f / (1.0f + expf(-(r.conf - tau) / a.T));
+  }
+  return r;
+}
+
+// Blend coefficients of target t of pair (fa, fb) for one bin (eq:fcpasm with
+// the orthonormal normalisation folded in): A_t = (1-alpha) e^{i g alpha theta} /
+// (H W), B_t = alpha e^{-i g (1-alpha) theta} / (H W), alpha = (t - fa)/(fb - fa).
+__device__ __forceinline__ float4 blend_coef(int t, int fa, int fb, float theta, float gate,
+                                             int H, int W, bool active) {
+  if (!active) return make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  const float alpha = (float)(t - fa) * (1.0f / (float)(fb - fa));
+  const float nrm = 1.0f / (float)(H * W);
+  float sa, ca, sb, cb;
+  sincosf(gate * alpha * theta, &sa, &ca);
+  sincosf(-gate * (1.0f - alpha) * theta, &sb, &cb);
+  const float wa = (1.0f - alpha) * nrm, wb = alpha * nrm;
+  return make_float4(wa * ca, wa * sa, wb * cb, wb * sb);
+}
+
+// ---------------------------------------------------------------------------
 // par_recon
 // ---------------------------------------------------------------------------
 // Number of unique stored bins of an HP x WP tile (Hermitian columns keep ky <= HP/2).
@@ -260,13 +365,38 @@ __device__ __forceinline__ void anchor_tile_update(const ParArgs& a, const float
 // (nontemporal loads and stores).  With several anchor pairs this pass reads every
 // interior anchor once per adjacent pair, and streaming the targets keeps those
 // anchors in the Infinity Cache for the second read.
-template <int HP, int WP, bool ACC, bool NTT>
+//
+// INL: the wave computes its tile's gate itself (bin_gate, one lane per stored bin,
+// from the cross-spectrum partials) and each target's blend coefficients into
+// coef_lds, instead of reading those of par_gate.  For grids that the chip holds
+// in one round, where the gate launch would be a serial step of its own.
+template <int HP, int WP, bool ACC, bool NTT, bool INL = false>
 __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __restrict__ resid,
                                            float* __restrict__ out,
                                            const float4* __restrict__ coef, const TileGeom& g,
-                                           int tile, int c_lane, int pair, float* fb_lds) {
+                                           int tile, int c_lane, int pair, float* fb_lds,
+                                           const float* __restrict__ partial = nullptr,
+                                           float4* coef_lds = nullptr) {
   constexpr int NKX = WP / 2 + 1;
   constexpr int NU = unique_bins<HP, WP>();
+  // INL: this lane's bin slot and its gate (lanes past the tile's bins: inactive)
+  BinSlot bs{};
+  BinGate bg{};
+  if constexpr (INL) {
+    bs = bin_slot((int)(threadIdx.x & 63), HP, WP);
+    float zr = 0.0f, zi = 0.0f, w = 0.0f;
+    if (bs.active) {
+      const float* src = partial + ((long long)pair * a.n_tiles + tile) * a.n_chblk * kVals +
+                         (bs.sky * kNkx + bs.kx) * 3;
+#pragma unroll 8
+      for (int j = 0; j < a.n_chblk; ++j) {
+        zr += src[(long long)j * kVals + 0];
+        zi += src[(long long)j * kVals + 1];
+        w += src[(long long)j * kVals + 2];
+      }
+    }
+    bg = bin_gate(a, bs, HP, WP, zr, zi, w);
+  }
   // Lanes past the last channel mirror channel D-1: same inputs, same results, and
   // they sit in the same wave as the lane that owns D-1, so their stores (and
   // read-modify-writes) coincide with it instruction by instruction.
@@ -310,6 +440,16 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
     else { if (pair != n_pairs - 1) continue; t0 = fb + 1; t1 = a.n_frames; }
     for (int t = t0; t < t1; ++t) {
       const float4* __restrict__ cf = coef + ((long long)t * a.n_tiles + tile) * kBins;
+      if constexpr (INL) {
+        // this target's coefficients, one bin per lane, into LDS for every lane
+        const int b = (int)(threadIdx.x & 63);
+        if (b < kBins) coef_lds[b] = blend_coef(t, fa, fb, bg.theta, bg.gate, HP, WP, bs.active);
+        __syncthreads();
+      }
+      auto coef_at = [&](int u) -> float4 {
+        if constexpr (INL) return coef_lds[u];
+        else return cf[u];
+      };
       const __amdgpu_buffer_rsrc_t dst = frame_rsrc(out, t, a.frame_elems);
       // Recompute the uniform token offsets per target instead of keeping 64 of them
       // live across the target loop.
@@ -341,7 +481,7 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
           fft::static_for<0, HP / 2 + 1>([&](auto yy) {
             constexpr int ky = decltype(yy)::value;
             constexpr int u = unique_slot<HP, WP>(ky, kx);
-            const float4 k = cf[ky * kNkx + kx];
+            const float4 k = coef_at(ky * kNkx + kx);
             if constexpr (self_conj(ky, kx, HP, WP)) {
               hr[ky] = k.x * ar[ky][kx] + k.z * fbr(u);
               hi[ky] = 0.0f;
@@ -362,7 +502,7 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
           fft::static_for<0, HP>([&](auto yy) {
             constexpr int ky = decltype(yy)::value;
             constexpr int u = unique_slot<HP, WP>(ky, kx);
-            const float4 k = cf[ky * kNkx + kx];
+            const float4 k = coef_at(ky * kNkx + kx);
             const float b_r = fbr(u), b_i = fbi(u);
             hr[ky] = k.x * ar[ky][kx] - k.y * ai[ky][kx] + k.z * b_r - k.w * b_i;
             hi[ky] = k.x * ai[ky][kx] + k.y * ar[ky][kx] + k.z * b_i + k.w * b_r;
@@ -392,13 +532,15 @@ __device__ __forceinline__ void recon_body(const ParArgs& a, const float* __rest
 }
 
 // One block of the reconstruction pass: tile `tile`, channel block `chb`, pair.
-template <int HP, int WP, bool ACC, bool NTT>
+template <int HP, int WP, bool ACC, bool NTT, bool INL = false>
 __device__ __forceinline__ void recon_block(const ParArgs& a, int tile, int chb, int pair,
                                             const float* __restrict__ resid, float* __restrict__ out,
-                                            const float4* __restrict__ coef, float* fb_lds) {
+                                            const float4* __restrict__ coef, float* fb_lds,
+                                            const float* __restrict__ partial = nullptr,
+                                            float4* coef_lds = nullptr) {
   const TileGeom g = tile_geom(a, tile);
-  recon_body<HP, WP, ACC, NTT>(a, resid, out, coef, g, tile, chb * kChb + threadIdx.x, pair,
-                          fb_lds + threadIdx.x);
+  recon_body<HP, WP, ACC, NTT, INL>(a, resid, out, coef, g, tile, chb * kChb + threadIdx.x, pair,
+                                    fb_lds + threadIdx.x, partial, coef_lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -461,29 +603,32 @@ __global__ __launch_bounds__(64) void par_xspec_fused(ParArgs a, ClassSet cs,
   });
 }
 
-template <int HR, int WR, bool ACC, bool NTT>
+template <int HR, int WR, bool ACC, bool NTT, bool INL>
 __global__ __launch_bounds__(64) void par_recon_fused(ParArgs a, ClassSet cs,
                                                        const float* __restrict__ resid,
                                                        float* __restrict__ out,
-                                                       const float4* __restrict__ coef) {
+                                                       const float4* __restrict__ coef,
+                                                       const float* __restrict__ partial) {
   __shared__ float fb_lds[2 * kBins * kChb];
+  __shared__ float4 coef_lds[INL ? kBins : 1];
   int tile_b, chb, pair;
   fused_block_work(blockIdx.x, cs.end[3], a.n_chblk, tile_b, chb, pair);
   pair = a.recon_order[pair];
   for_class<HR, WR>(a, cs, tile_b, [&](auto hp, auto wp, int tile) {
-    recon_block<decltype(hp)::value, decltype(wp)::value, ACC, NTT>(a, tile, chb, pair, resid, out,
-                                                                   coef, fb_lds);
+    recon_block<decltype(hp)::value, decltype(wp)::value, ACC, NTT, INL>(
+        a, tile, chb, pair, resid, out, coef, fb_lds, partial, coef_lds);
   });
 }
 
 typedef void (*XspecFusedFn)(ParArgs, ClassSet, const float*, float*);
-typedef void (*ReconFusedFn)(ParArgs, ClassSet, const float*, float*, const float4*);
+typedef void (*ReconFusedFn)(ParArgs, ClassSet, const float*, float*, const float4*, const float*);
 
 // The fused kernels of one bottom-remainder height HR, for WR = 1..8
 // (each row is compiled in its own translation unit).
 struct FusedRow {
   XspecFusedFn xspec[8];
   ReconFusedFn recon_w[8], recon_a[8], recon_as[8];   // write, accumulate, accumulate streaming
+  ReconFusedFn inl_w[8], inl_a[8], inl_as[8];         // the same with the gate computed inline
 };
 
 void fused_row_1(FusedRow& r);

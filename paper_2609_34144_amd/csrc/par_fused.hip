@@ -16,9 +16,12 @@ namespace pardev {
 template <int HR, int WR>
 static void set_entry(FusedRow& r) {
   r.xspec[WR - 1] = par_xspec_fused<HR, WR>;
-  r.recon_w[WR - 1] = par_recon_fused<HR, WR, false, false>;
-  r.recon_a[WR - 1] = par_recon_fused<HR, WR, true, false>;
-  r.recon_as[WR - 1] = par_recon_fused<HR, WR, true, true>;
+  r.recon_w[WR - 1] = par_recon_fused<HR, WR, false, false, false>;
+  r.recon_a[WR - 1] = par_recon_fused<HR, WR, true, false, false>;
+  r.recon_as[WR - 1] = par_recon_fused<HR, WR, true, true, false>;
+  r.inl_w[WR - 1] = par_recon_fused<HR, WR, false, false, true>;
+  r.inl_a[WR - 1] = par_recon_fused<HR, WR, true, false, true>;
+  r.inl_as[WR - 1] = par_recon_fused<HR, WR, true, true, true>;
 }
 
 void CAST_CAT(fused_row_, CAST_PAR_HR)(FusedRow& r) {

@@ -488,6 +488,44 @@ def test_par_workspace_reuse_and_long_target_runs(cast_lib):
         assert rr <= PAR_REL_RMS, (j, rr)
 
 
+def test_par_gate_inline_and_launched(cast_lib):
+    """Reconstruction grids that the chip holds in one round take the gate inside
+    the reconstruction blocks; asking for a debug output (conf_out here) takes the
+    gate launch instead.  Both must meet the PAR bar and agree with each other to
+    fp32 rounding (their channel sums run in different orders), in write and
+    accumulate mode, with one and with several anchor pairs."""
+    dev = "cuda"
+    rng = np.random.default_rng(21)
+    for (n, Hg, Wg, D, anchors) in [(8, 30, 52, 192, (0, 3, 7)), (6, 13, 11, 70, (1, 4)),
+                                    (9, 16, 16, 64, (0, 2, 5, 8))]:
+        base = rng.standard_normal((Hg, Wg, D))
+        resid = np.zeros((n, Hg, Wg, D))
+        for j, a in enumerate(anchors):
+            resid[a] = np.roll(base, (j, -j), axis=(0, 1)) + 0.3 * rng.standard_normal((Hg, Wg, D))
+        r = torch.from_numpy(resid.astype(np.float32)).to(dev)
+        for acc in (False, True):
+            x0 = rng.standard_normal(resid.shape)
+            prm = cast_lib.cast_par_params_default(accumulate=int(acc))
+            _, s2 = cast_lib.par_debug_shapes(len(anchors), Hg, Wg, prm)
+            outs = []
+            for launched in (False, True):
+                out = torch.from_numpy(x0.astype(np.float32)).to(dev)
+                conf = torch.zeros(s2, device=dev) if launched else None
+                cast_lib.cast_par_reconstruct(r, anchors, prm, out=out, conf_out=conf)
+                torch.cuda.synchronize()
+                outs.append(out.cpu().numpy().astype(np.float64))
+            ref = OP.par_reconstruct(resid.astype(np.float32).astype(np.float64), anchors,
+                                     OP.ParParams(accumulate=acc),
+                                     out=x0.astype(np.float32).astype(np.float64) if acc else None)
+            sk = [t for t in range(n) if t not in set(anchors)]
+            base_t = x0[sk] if acc else 0.0
+            for o in outs:
+                assert rel_rms(o[sk], ref[sk]) <= PAR_REL_RMS
+            d = rel_rms(outs[0][sk] - base_t, outs[1][sk] - base_t)
+            log(f"[par gate inline vs launched {Hg}x{Wg}x{D} acc {acc}] rel-RMS {d:.2e}")
+            assert d <= 1e-5, d
+
+
 def test_par_tiny_all_modes(cast_lib):
     w = gen.get(W.TINY)
     resid, x0, _ = gen.par_inputs(w, seed=42)
